@@ -1,0 +1,299 @@
+// Host side of the C ABI declared in include/art.h: argument checks, the
+// launch plan (a function of the shape only), the workspace layout, the
+// per-call epoch and the checked-mode validator.
+#include "art.h"
+
+#include <math.h>
+#include <string.h>
+
+#include <atomic>
+#include <vector>
+
+#include "art_internal.h"
+
+namespace {
+
+using art::Plan;
+using art::KernelParams;
+
+constexpr size_t kAlign = 256;
+constexpr uint32_t kSpinLimit = 1u << 22;  // polls (~seconds) before a wait gives up
+
+// Process-wide call counter: every launch tags the flags it writes with a
+// fresh value, so flags left by earlier calls are never mistaken for current.
+std::atomic<uint64_t> g_epoch{0};
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int ilog2(int64_t x) {
+    int r = 0;
+    while ((int64_t(1) << r) < x) ++r;
+    return r;
+}
+
+art_status check_shape(const art_decode_shape* s, const art_decode_opts* o) {
+    if (!s || !o) return ART_ERR_INVALID_ARG;
+    if (s->batch < 0 || s->num_kv_heads <= 0 || s->num_q_heads <= 0 ||
+        s->num_q_heads % s->num_kv_heads != 0 || s->head_dim <= 0 || s->block_size <= 0 ||
+        s->page_size <= 0 || s->num_pages <= 0 || s->max_pages_per_seq <= 0 ||
+        s->max_blocks_per_list < 0 || (s->list_per_head != 0 && s->list_per_head != 1))
+        return ART_ERR_INVALID_ARG;
+    if (s->k_stride_page < 0 || s->k_stride_head < 0 || s->k_stride_token < 0 ||
+        s->v_stride_page < 0 || s->v_stride_head < 0 || s->v_stride_token < 0)
+        return ART_ERR_INVALID_ARG;
+    if (isnan(o->tau) || isnan(o->phi) || !isfinite(o->softmax_scale) || o->patience < 1 ||
+        (o->dense_order != ART_ORDER_RECENT_FIRST && o->dense_order != ART_ORDER_FORWARD) ||
+        (o->out_dtype != ART_OUT_F32 && o->out_dtype != ART_OUT_BF16) || o->chunk_blocks < 0 ||
+        o->chunk_blocks > art::kMaxChunkTiles)
+        return ART_ERR_INVALID_ARG;
+    const int g = s->num_q_heads / s->num_kv_heads;
+    if (s->head_dim != art::kHeadDim) return ART_ERR_UNSUPPORTED;
+    if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return ART_ERR_UNSUPPORTED;
+    if (s->block_size % art::kTile != 0 || s->block_size / art::kTile > art::kMaxChunkTiles)
+        return ART_ERR_UNSUPPORTED;
+    if (!is_pow2(s->page_size) || s->page_size < 16) return ART_ERR_UNSUPPORTED;
+    // 16-byte vector loads of 8 head dims need 8-element aligned rows
+    if (s->k_stride_page % 8 || s->k_stride_head % 8 || s->k_stride_token % 8 ||
+        s->v_stride_page % 8 || s->v_stride_head % 8 || s->v_stride_token % 8)
+        return ART_ERR_UNSUPPORTED;
+    return ART_OK;
+}
+
+// Everything about the launch is decided here from the shape (and the
+// chunk_blocks option): never from the data or the thresholds.
+art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* p) {
+    art_status st = check_shape(s, o);
+    if (st != ART_OK) return st;
+    const int g = s->num_q_heads / s->num_kv_heads;
+    const int tpb = s->block_size / art::kTile;
+    const int64_t cap_tokens = (int64_t)s->max_pages_per_seq * s->page_size;
+    const int64_t t_dense = (cap_tokens + s->block_size - 1) / s->block_size;
+    int64_t t_cap = t_dense > s->max_blocks_per_list ? t_dense : s->max_blocks_per_list;
+    if (t_cap < 1) t_cap = 1;
+    if (t_cap > INT32_MAX / 2) return ART_ERR_UNSUPPORTED;
+    const int64_t n_groups = (int64_t)s->batch * s->num_kv_heads;
+
+    const int rec_tile = g * art::kHeadDim + 2 * g;                 // floats
+    const size_t pbuf_bytes = (size_t)art::kWaves * art::kTile * g * 4;
+    const size_t lds_cap = 64 * 1024;
+    int max_tiles = art::kMaxChunkTiles;
+    while (max_tiles > tpb && (size_t)max_tiles * rec_tile * 4 + pbuf_bytes > lds_cap) --max_tiles;
+    if ((size_t)tpb * rec_tile * 4 + pbuf_bytes > lds_cap) return ART_ERR_UNSUPPORTED;
+    const int c_max = max_tiles / tpb;
+
+    int C;
+    if (o->chunk_blocks > 0) {
+        C = o->chunk_blocks;
+    } else {
+        // about 8 tiles (two per wavefront) per chunk; smaller chunks when
+        // the whole problem would not give the 256 CUs enough workgroups
+        C = 8 / tpb;
+        if (C < 1) C = 1;
+        while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
+    }
+    if (C > c_max) C = c_max;
+    if (C < 1) C = 1;
+    const int64_t max_chunks = (t_cap + C - 1) / C;
+    if (n_groups * max_chunks > INT32_MAX) return ART_ERR_UNSUPPORTED;
+
+    p->group = g;
+    p->tiles_per_block = tpb;
+    p->chunk_blocks = C;
+    p->max_chunks = (int32_t)max_chunks;
+    p->n_groups = (int32_t)n_groups;
+    p->t_cap = (int32_t)t_cap;
+    p->record_floats = (g * art::kHeadDim + 2 * g + 63) / 64 * 64;
+    p->lds_bytes = (size_t)C * tpb * rec_tile * 4 + pbuf_bytes;
+
+    art::WorkspaceLayout& w = p->ws;
+    size_t off = 0;
+    w.error_off = off;      off = align_up(off + 4);
+    w.claim_off = off;      off = align_up(off + 4 * (size_t)n_groups);
+    w.stop_epoch_off = off; off = align_up(off + 8 * (size_t)n_groups);
+    w.stop_chunk_off = off; off = align_up(off + 4 * (size_t)n_groups);
+    w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
+    w.stab_off = off;       off = align_up(off + 32 * (size_t)n_groups * max_chunks);
+    w.records_off = off;    off = align_up(off + (size_t)n_groups * max_chunks * 2 * p->record_floats * 4);
+    w.total = off;
+    return ART_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t art_abi_version(void) { return ART_ABI_VERSION; }
+
+const char* art_status_str(int32_t status) {
+    switch (status) {
+        case ART_OK: return "ART_OK";
+        case ART_ERR_INVALID_ARG: return "ART_ERR_INVALID_ARG";
+        case ART_ERR_UNSUPPORTED: return "ART_ERR_UNSUPPORTED";
+        case ART_ERR_WORKSPACE_TOO_SMALL: return "ART_ERR_WORKSPACE_TOO_SMALL";
+        case ART_ERR_HIP: return "ART_ERR_HIP";
+        case ART_ERR_BAD_INDEX: return "ART_ERR_BAD_INDEX";
+        case ART_ERR_DEVICE_TIMEOUT: return "ART_ERR_DEVICE_TIMEOUT";
+        default: return "ART_ERR_UNKNOWN";
+    }
+}
+
+size_t art_decode_workspace_bytes(const art_decode_shape* shape, const art_decode_opts* opts,
+                                  int32_t* status) {
+    Plan p;
+    art_status st = make_plan(shape, opts, &p);
+    if (status) *status = st;
+    return st == ART_OK ? p.ws.total : 0;
+}
+
+art_status art_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
+    if (!workspace && bytes) return ART_ERR_INVALID_ARG;
+    if (bytes % 4) return ART_ERR_INVALID_ARG;
+    return art::launch_fill_zero(workspace, bytes, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
+}
+
+art_status art_decode_attention(const art_decode_shape* shape, const art_decode_opts* opts,
+                                const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* page_table, const int32_t* seq_lens,
+                                const int32_t* block_list, const int32_t* block_list_len,
+                                void* out, float* lse, int32_t* stop_block,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    Plan plan;
+    art_status st = make_plan(shape, opts, &plan);
+    if (st != ART_OK) return st;
+    if (shape->batch == 0) return ART_OK;
+    if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !out || !lse || !stop_block)
+        return ART_ERR_INVALID_ARG;
+    if ((block_list == nullptr) != (block_list_len == nullptr)) return ART_ERR_INVALID_ARG;
+    if (block_list && shape->max_blocks_per_list <= 0) return ART_ERR_INVALID_ARG;
+    if (((uintptr_t)q | (uintptr_t)k_cache | (uintptr_t)v_cache | (uintptr_t)out) % 16)
+        return ART_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < plan.ws.total) return ART_ERR_WORKSPACE_TOO_SMALL;
+    if ((uintptr_t)workspace % 8) return ART_ERR_INVALID_ARG;
+
+    KernelParams k;
+    memset(&k, 0, sizeof k);
+    k.batch = shape->batch;
+    k.num_q_heads = shape->num_q_heads;
+    k.num_kv_heads = shape->num_kv_heads;
+    k.block_size = shape->block_size;
+    k.page_shift = ilog2(shape->page_size);
+    k.num_pages = shape->num_pages;
+    k.max_pages = shape->max_pages_per_seq;
+    k.max_list = shape->max_blocks_per_list;
+    k.list_per_head = shape->list_per_head;
+    k.ks_page = shape->k_stride_page;
+    k.ks_head = shape->k_stride_head;
+    k.ks_tok = shape->k_stride_token;
+    k.vs_page = shape->v_stride_page;
+    k.vs_head = shape->v_stride_head;
+    k.vs_tok = shape->v_stride_token;
+    k.scale_log2 = (float)((double)opts->softmax_scale * 1.4426950408889634);
+    k.tau = opts->tau;
+    k.phi = opts->phi;
+    k.patience = opts->patience;
+    k.dense_order = opts->dense_order;
+    k.out_bf16 = opts->out_dtype == ART_OUT_BF16;
+    k.tiles_per_block = plan.tiles_per_block;
+    k.chunk_blocks = plan.chunk_blocks;
+    k.max_chunks = plan.max_chunks;
+    k.t_cap = plan.t_cap;
+    k.record_floats = plan.record_floats;
+    k.chunk_tiles_lds = plan.chunk_blocks * plan.tiles_per_block;
+    k.q = static_cast<const uint16_t*>(q);
+    k.k = static_cast<const uint16_t*>(k_cache);
+    k.v = static_cast<const uint16_t*>(v_cache);
+    k.page_table = page_table;
+    k.seq_lens = seq_lens;
+    k.block_list = block_list;
+    k.block_list_len = block_list_len;
+    k.out = out;
+    k.lse = lse;
+    k.stop_block = stop_block;
+    char* ws = static_cast<char*>(workspace);
+    k.error_word = reinterpret_cast<uint32_t*>(ws + plan.ws.error_off);
+    k.claim = reinterpret_cast<uint32_t*>(ws + plan.ws.claim_off);
+    k.stop_epoch = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_epoch_off);
+    k.stop_chunk = reinterpret_cast<uint32_t*>(ws + plan.ws.stop_chunk_off);
+    k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
+    k.stab = reinterpret_cast<int32_t*>(ws + plan.ws.stab_off);
+    k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
+    k.epoch = g_epoch.fetch_add(1, std::memory_order_relaxed) + 1;
+    k.spin_limit = kSpinLimit;
+    if (k.epoch >= (uint64_t(1) << 60)) return ART_ERR_UNSUPPORTED;
+    return art::launch_decode(plan, k, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
+}
+
+art_status art_validate_inputs(const art_decode_shape* shape, const art_decode_opts* opts,
+                               const int32_t* page_table, const int32_t* seq_lens,
+                               const int32_t* block_list, const int32_t* block_list_len,
+                               hipStream_t stream, int64_t* bad_index, int32_t* bad_where) {
+    if (bad_index) *bad_index = -1;
+    if (bad_where) *bad_where = -1;
+    art_status st = check_shape(shape, opts);
+    if (st != ART_OK) return st;
+    const int B = shape->batch;
+    if (B == 0) return ART_OK;
+    if (!page_table || !seq_lens || ((block_list == nullptr) != (block_list_len == nullptr)))
+        return ART_ERR_INVALID_ARG;
+    const int rows = shape->list_per_head ? shape->num_kv_heads : 1;
+    std::vector<int32_t> sl(B), pt((size_t)B * shape->max_pages_per_seq), bll, bl;
+    if (hipMemcpyAsync(sl.data(), seq_lens, sizeof(int32_t) * B, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipMemcpyAsync(pt.data(), page_table, sizeof(int32_t) * pt.size(), hipMemcpyDeviceToHost, stream) != hipSuccess)
+        return ART_ERR_HIP;
+    if (block_list) {
+        bll.resize((size_t)B * rows);
+        bl.resize((size_t)B * rows * shape->max_blocks_per_list);
+        if (hipMemcpyAsync(bll.data(), block_list_len, sizeof(int32_t) * bll.size(), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+            (!bl.empty() && hipMemcpyAsync(bl.data(), block_list, sizeof(int32_t) * bl.size(), hipMemcpyDeviceToHost, stream) != hipSuccess))
+            return ART_ERR_HIP;
+    }
+    if (hipStreamSynchronize(stream) != hipSuccess) return ART_ERR_HIP;
+    auto fail = [&](int64_t idx, int32_t where) {
+        if (bad_index) *bad_index = idx;
+        if (bad_where) *bad_where = where;
+        return ART_ERR_BAD_INDEX;
+    };
+    const int64_t cap = (int64_t)shape->max_pages_per_seq * shape->page_size;
+    for (int b = 0; b < B; ++b)
+        if (sl[b] < 0 || sl[b] > cap) return fail(b, 0);
+    for (int b = 0; b < B; ++b) {
+        const int64_t npg = ((int64_t)sl[b] + shape->page_size - 1) / shape->page_size;
+        for (int64_t i = 0; i < npg; ++i) {
+            const int32_t pg = pt[(size_t)b * shape->max_pages_per_seq + i];
+            if (pg < 0 || pg >= shape->num_pages) return fail((int64_t)b * shape->max_pages_per_seq + i, 1);
+        }
+    }
+    if (block_list) {
+        std::vector<uint8_t> seen;
+        for (int b = 0; b < B; ++b) {
+            const int64_t nblk = ((int64_t)sl[b] + shape->block_size - 1) / shape->block_size;
+            for (int r = 0; r < rows; ++r) {
+                const int64_t row = (int64_t)b * rows + r;
+                const int32_t n = bll[row];
+                if (n < 0 || n > shape->max_blocks_per_list) return fail(row, 3);
+                seen.assign((size_t)(nblk > 0 ? nblk : 1), 0);
+                for (int32_t i = 0; i < n; ++i) {
+                    const int64_t idx = row * shape->max_blocks_per_list + i;
+                    const int32_t id = bl[idx];
+                    if (id < 0 || id >= nblk || seen[id]) return fail(idx, 2);
+                    seen[id] = 1;
+                }
+            }
+        }
+    }
+    return ART_OK;
+}
+
+art_status art_workspace_status(const void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                int32_t* device_status) {
+    if (!workspace || workspace_bytes < 4 || !device_status) return ART_ERR_INVALID_ARG;
+    uint32_t word = 0;
+    if (hipStreamSynchronize(stream) != hipSuccess) return ART_ERR_HIP;
+    if (hipMemcpy(&word, workspace, 4, hipMemcpyDeviceToHost) != hipSuccess) return ART_ERR_HIP;
+    *device_status = word == 0 ? ART_OK : (word == 7 ? ART_ERR_INVALID_ARG : ART_ERR_DEVICE_TIMEOUT);
+    return ART_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// Internal declarations shared by the host API (art_api.cpp) and the kernels
+// (art_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+namespace art {
+
+constexpr int kHeadDim = 128;   // dims per head (the only supported value)
+constexpr int kTile = 64;       // tokens one wavefront processes per tile
+constexpr int kWaves = 4;       // wavefronts per workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxChunkTiles = 16;
+
+// Progress of one chunk, published in the low 3 bits of its flag word (the
+// rest of the word holds the call's epoch).  States only ever increase.
+enum ChunkState : uint32_t {
+    kNone = 0,
+    kAggregate = 1,      // softmax aggregate of the chunk's own blocks
+    kInclusive = 2,      // softmax state after the chunk (inclusive prefix)
+    kStabSummary = 3,    // stability summary of the chunk's own blocks
+    kStabInclusive = 4,  // stop/patience state after the chunk
+};
+
+// Byte layout of a workspace (all offsets from its start, 256-aligned).
+struct WorkspaceLayout {
+    size_t error_off;        // uint32 error word
+    size_t claim_off;        // uint32 [groups] chunk-claim counters
+    size_t stop_epoch_off;   // uint64 [groups] epoch of the announced stop
+    size_t stop_chunk_off;   // uint32 [groups] chunk that holds the stop
+    size_t flags_off;        // uint64 [groups][max_chunks]
+    size_t stab_off;         // int32 [groups][max_chunks][8]
+    size_t records_off;      // float [groups][max_chunks][2][record_floats]
+    size_t total;
+};
+
+struct Plan {
+    int32_t group;           // query heads per KV head (g)
+    int32_t tiles_per_block; // block_size / kTile
+    int32_t chunk_blocks;    // blocks per chunk (C)
+    int32_t max_chunks;      // chunks per group the grid provides
+    int32_t n_groups;        // batch * num_kv_heads
+    int32_t t_cap;           // traversal length bound per group
+    int32_t record_floats;   // floats per aggregate / inclusive record
+    size_t lds_bytes;        // dynamic LDS per workgroup
+    WorkspaceLayout ws;
+};
+
+// Everything the kernel reads, passed by value.
+struct KernelParams {
+    // shape
+    int32_t batch, num_q_heads, num_kv_heads, block_size, page_shift, num_pages;
+    int32_t max_pages, max_list, list_per_head;
+    int64_t ks_page, ks_head, ks_tok, vs_page, vs_head, vs_tok;
+    // options
+    float scale_log2;        // softmax_scale * log2(e): scores kept in base 2
+    float tau, phi;
+    int32_t patience, dense_order, out_bf16;
+    // plan
+    int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
+    int32_t chunk_tiles_lds; // tile records that fit in dynamic LDS
+    // data
+    const uint16_t* q;
+    const uint16_t* k;
+    const uint16_t* v;
+    const int32_t* page_table;
+    const int32_t* seq_lens;
+    const int32_t* block_list;
+    const int32_t* block_list_len;
+    void* out;
+    float* lse;
+    int32_t* stop_block;
+    // workspace
+    uint32_t* error_word;
+    uint32_t* claim;
+    uint64_t* stop_epoch;
+    uint32_t* stop_chunk;
+    uint64_t* flags;
+    int32_t* stab;
+    float* records;
+    uint64_t epoch;          // unique per call; tags every flag it writes
+    uint32_t spin_limit;     // polls before a wait gives up
+};
+
+// Launchers (art_kernels.hip).  Return a hipError_t.
+int launch_decode(const Plan& plan, const KernelParams& params, hipStream_t stream);
+int launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace art

@@ -1,0 +1,788 @@
+// ART decode attention kernels for gfx950 (MI355X).
+//
+// One launch computes, for every (sequence b, KV head kvh) group, the
+// block-streaming softmax attention of Sec. 3.1 over the group's traversal
+// (recency-first, forward, or a supplied block list, Sec. 3.4), the
+// magnitude/direction stability test of Sec. 3.2 (Eq. 2) after every block,
+// the patience counter of Eq. (3) and the early break of Algorithm 1.
+//
+// Work decomposition
+//   A group's traversal of T blocks is cut into chunks of C consecutive
+//   blocks.  One workgroup (4 wavefronts) handles one chunk; the grid is
+//   chunk-major (blockIdx = chunk_hint * groups + group) so that the early
+//   chunks of every group are dispatched first.  The order in which a
+//   group's chunks start is fixed by a per-group claim counter, so a chunk
+//   only ever waits on chunks that are already running: no deadlock whatever
+//   the dispatch order.
+//
+//   Phase 1 (all 4 waves): each wave streams 64-token tiles of the chunk's
+//   blocks from HBM (16-byte loads, four 64-byte row segments per K load
+//   instruction, four 256-byte rows per V load instruction), computes the
+//   scores of all g query heads with v_mfma_f32_16x16x32_bf16 (query heads
+//   are the M rows, tokens the N columns, head dims the reduction), the tile
+//   softmax in base 2 with row reductions over DPP, and P.V on the VALU in
+//   fp32, and leaves (m, l, sum p v) for its tile in LDS.
+//
+//   Phase 2 (wave 0 only; the other waves retire):
+//     - folds the tiles into block partials and the chunk aggregate and
+//       publishes the aggregate;
+//     - obtains the softmax state after the previous chunk by looking back
+//       to the nearest chunk that published its inclusive state and folding
+//       the aggregates in between forward.  Because the fold is always
+//       left-to-right over the same aggregates, every chunk computes the
+//       same bits for a given prefix: results do not depend on timing;
+//     - replays its blocks from that prefix, running the stability test per
+//       block (normalised running output o(t), increment d = o(t) - o(t-1),
+//       d_scale = |d|, d_direction = 1 - cos from |o|^2, |d|^2 and o.d
+//       without cancellation);
+//     - publishes a stability summary, looks back the same way over the
+//       stability states (entering patience run, stop already found), and
+//       either stops inside the chunk (writes out/lse/stop_block and
+//       announces the stop so that later chunks skip their loads), or, as
+//       the last chunk, writes the untruncated result.
+//   Cross-workgroup data goes through the workspace with agent-scope
+//   release/acquire, as the XCDs of MI355X have separate L2 caches.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "art_internal.h"
+
+namespace art {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kNegInf = -__builtin_inff();
+constexpr int kD = kHeadDim;
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;  // NaN
+  u += 0x7fffu + ((u >> 16) & 1u);                       // round to nearest even
+  return u >> 16;
+}
+
+// ---- wavefront reductions over the 16 lanes of a DPP row -------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kQuadXor1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kRowHalfMirror = 0x141; // lane i <- lane 7-i within each 8
+constexpr int kRowMirror = 0x140;     // lane i <- lane 15-i within each 16
+
+// Every lane of the row ends with the same bits (each step adds the same two
+// partial sums, only in swapped operand order).
+__device__ __forceinline__ float row_sum(float x) {
+  x = x + dpp_f<kQuadXor1>(x);
+  x = x + dpp_f<kQuadXor2>(x);
+  x = x + dpp_f<kRowHalfMirror>(x);
+  x = x + dpp_f<kRowMirror>(x);
+  return x;
+}
+__device__ __forceinline__ float row_max(float x) {
+  x = fmaxf(x, dpp_f<kQuadXor1>(x));
+  x = fmaxf(x, dpp_f<kQuadXor2>(x));
+  x = fmaxf(x, dpp_f<kRowHalfMirror>(x));
+  x = fmaxf(x, dpp_f<kRowMirror>(x));
+  return x;
+}
+
+// LDS written by some lanes of this wave, read by others.  LDS operations of
+// one wavefront complete in order; this waits for them and keeps the
+// compiler from moving memory operations across.
+__device__ __forceinline__ void wave_lds_sync() {
+  __asm__ __volatile__("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  __asm__ __volatile__("" ::: "memory");
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---- workspace flags ---------------------------------------------------------
+__device__ __forceinline__ uint64_t ld_relaxed(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_relaxed32(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+__device__ __forceinline__ void release_agent() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+
+__device__ __forceinline__ uint32_t flag_state(uint64_t v, uint64_t epoch) {
+  return (v >> 3) == epoch ? (uint32_t)(v & 7u) : 0u;
+}
+
+template <int G>
+struct Cfg {
+  static constexpr int HPL = G >= 4 ? G / 4 : 1;   // head slots per lane (state layout)
+  static constexpr int HC = G > 8 ? 8 : G;          // heads per P.V pass
+  static constexpr int REC = G * kD + 2 * G;        // floats per LDS tile record
+};
+
+// Per-head softmax state in the "state layout": lane l covers dims
+// 8*(l&15) .. +7 of heads (l>>4) + 4*k, k < HPL.  m is in base 2
+// (scores * scale * log2 e), L is the mass sum 2^(s - m), o the normalised
+// output.  L == 0 is the empty state.
+template <int G>
+struct State {
+  float m[Cfg<G>::HPL];
+  float L[Cfg<G>::HPL];
+  float o[Cfg<G>::HPL][8];
+};
+
+template <int G>
+__device__ __forceinline__ void state_clear(State<G>& s) {
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    s.m[k] = kNegInf;
+    s.L[k] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s.o[k][e] = 0.f;
+  }
+}
+
+template <int G>
+__device__ __forceinline__ bool slot_valid(int lane, int k) {
+  return ((lane >> 4) + 4 * k) < G;
+}
+
+// s <- s (+) p : softmax-weighted merge of two disjoint token sets.
+// o_new = o + w (o_p - o) with w = mass_p / (mass_s + mass_p) (the increment
+// form of Appendix A).  Written with explicit operations so that every call
+// site produces the same bits.  Optionally returns the increment d.
+template <int G, bool WANT_DELTA>
+__device__ __forceinline__ void merge(State<G>& s, const State<G>& p,
+                                      float (*delta)[8] = nullptr) {
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    const bool v1 = s.L[k] > 0.f;
+    const bool v2 = p.L[k] > 0.f;
+    const float mn = v1 ? (v2 ? fmaxf(s.m[k], p.m[k]) : s.m[k]) : p.m[k];
+    const float a = v1 ? __fmul_rn(s.L[k], fast_exp2(__fsub_rn(s.m[k], mn))) : 0.f;
+    const float bb = v2 ? __fmul_rn(p.L[k], fast_exp2(__fsub_rn(p.m[k], mn))) : 0.f;
+    const float Ln = __fadd_rn(a, bb);
+    const float w = v2 ? (v1 ? __fdiv_rn(bb, Ln) : 1.f) : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float d = __fmul_rn(w, __fsub_rn(p.o[k][e], s.o[k][e]));
+      if (WANT_DELTA) delta[k][e] = d;
+      s.o[k][e] = __fadd_rn(s.o[k][e], d);
+    }
+    s.m[k] = (v1 || v2) ? mn : kNegInf;
+    s.L[k] = Ln;
+  }
+}
+
+// ---- records: global (normalised state) and LDS tiles (unnormalised) ------
+template <int G>
+__device__ __forceinline__ void write_state(float* rec, const State<G>& s, int lane) {
+  const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    const int h = r + 4 * k;
+    if (h < G) {
+      f32x4* dst = reinterpret_cast<f32x4*>(rec + h * kD + c * 8);
+      dst[0] = f32x4{s.o[k][0], s.o[k][1], s.o[k][2], s.o[k][3]};
+      dst[1] = f32x4{s.o[k][4], s.o[k][5], s.o[k][6], s.o[k][7]};
+      if (c == 0) {
+        rec[G * kD + h] = s.m[k];
+        rec[G * kD + G + h] = s.L[k];
+      }
+    }
+  }
+}
+
+template <int G>
+__device__ __forceinline__ void read_state(const float* rec, State<G>& s, int lane) {
+  const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    int h = r + 4 * k;
+    if (h >= G) h = 0;  // idle slot: read something valid, never used
+    const f32x4* src = reinterpret_cast<const f32x4*>(rec + h * kD + c * 8);
+    const f32x4 x0 = src[0], x1 = src[1];
+    s.o[k][0] = x0[0]; s.o[k][1] = x0[1]; s.o[k][2] = x0[2]; s.o[k][3] = x0[3];
+    s.o[k][4] = x1[0]; s.o[k][5] = x1[1]; s.o[k][6] = x1[2]; s.o[k][7] = x1[3];
+    s.m[k] = rec[G * kD + h];
+    s.L[k] = rec[G * kD + G + h];
+  }
+}
+
+// An LDS tile record holds sum p v (not normalised); normalise on read.
+template <int G>
+__device__ __forceinline__ void read_tile(const float* rec, State<G>& s, int lane) {
+  read_state<G>(rec, s, lane);
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    const float inv = s.L[k] > 0.f ? __fdiv_rn(1.f, s.L[k]) : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s.o[k][e] = __fmul_rn(s.o[k][e], inv);
+  }
+}
+
+// ---- phase 1: one 64-token tile on one wavefront ---------------------------
+template <int G>
+__device__ __forceinline__ void load_q(const KernelParams& P, int b, int kvh, int lane, bf16x8 (&qa)[4]) {
+  const int h = lane & 15;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (h < G) {
+      const uint16_t* src = P.q + ((int64_t)b * P.num_q_heads + kvh * G + h) * kD + (4 * s + (lane >> 4)) * 8;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(src);
+      qa[s] = __builtin_bit_cast(bf16x8, w);
+    } else {
+      qa[s] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+}
+
+__device__ __forceinline__ int clamp_page(const KernelParams& P, int b, int tok) {
+  int pg = P.page_table[(int64_t)b * P.max_pages + (tok >> P.page_shift)];
+  pg = pg < 0 ? 0 : pg;
+  return pg >= P.num_pages ? P.num_pages - 1 : pg;
+}
+
+// Writes into `rec` (LDS): sum_j p_hj v_j [G][128], m_h [G] (base 2), l_h [G].
+template <int G>
+__device__ void compute_tile(const KernelParams& P, int b, int kvh, int L, int tok0,
+                             const bf16x8 (&qa)[4], float* __restrict__ pbuf,
+                             float* __restrict__ rec) {
+  const int lane = threadIdx.x & 63;
+  const int lo = lane & 15, hi = lane >> 4;
+  const int psz_mask = (1 << P.page_shift) - 1;
+
+  if (tok0 >= L) {  // tile past the sequence end: empty partial
+    for (int i = lane; i < G * kD; i += 64) rec[i] = 0.f;
+    if (lane < G) {
+      rec[G * kD + lane] = kNegInf;
+      rec[G * kD + G + lane] = 0.f;
+    }
+    return;
+  }
+
+  // K: for 16-token group n, lane holds token 16n + lo, dims chunk 4s + hi.
+  // A 16-aligned group never straddles a page (page_size >= 16, power of
+  // two); tokens past L are redirected to token L-1, which lies in the same
+  // group or in the last group before it, so one page serves the group.
+  u32x4 kr[4][4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) {
+    const int gt = min(tok0 + 16 * n, L - 1);
+    const int pg = clamp_page(P, b, gt);
+    const int tok = min(tok0 + 16 * n + lo, L - 1);
+    const uint16_t* kp = P.k + (int64_t)pg * P.ks_page + (int64_t)kvh * P.ks_head +
+                         (int64_t)(tok & psz_mask) * P.ks_tok;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      kr[n][s] = *reinterpret_cast<const u32x4*>(kp + (4 * s + hi) * 8);
+  }
+  // V: lane (lo, hi) holds tokens 16*hi + i, dims 8*lo .. +7.
+  u32x4 vr[16];
+  {
+    const int gt = min(tok0 + 16 * hi, L - 1);
+    const int pg = clamp_page(P, b, gt);
+    const uint16_t* vp = P.v + (int64_t)pg * P.vs_page + (int64_t)kvh * P.vs_head + lo * 8;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int tok = min(tok0 + 16 * hi + i, L - 1);
+      vr[i] = *reinterpret_cast<const u32x4*>(vp + (int64_t)(tok & psz_mask) * P.vs_tok);
+    }
+  }
+
+  // Scores: S[n] = Q (16 head rows) x K^T (16 token columns), K = 128 dims.
+  f32x4 S[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) {
+    S[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      S[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[s], __builtin_bit_cast(bf16x8, kr[n][s]), S[n], 0, 0, 0);
+  }
+  // S[n][r]: head 4*hi + r, token 16n + lo.
+  const int hb = 4 * hi;
+  float sc[4][4], mx[4], lsum[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float m = kNegInf;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const bool ok = (hb + r < G) && (tok0 + 16 * n + lo < L);
+      sc[n][r] = ok ? S[n][r] * P.scale_log2 : kNegInf;
+      m = fmaxf(m, sc[n][r]);
+    }
+    mx[r] = row_max(m);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float acc = 0.f;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const float p = mx[r] == kNegInf ? 0.f : fast_exp2(sc[n][r] - mx[r]);
+      sc[n][r] = p;
+      acc += p;
+    }
+    lsum[r] = row_sum(acc);
+  }
+  // p to LDS as [token][head] for the P.V layout.
+  if (hb < G) {
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (hb + r < G) pbuf[(16 * n + lo) * G + hb + r] = sc[n][r];
+  }
+  if (lo == 0 && hb < G) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (hb + r < G) {
+        rec[G * kD + hb + r] = mx[r];
+        rec[G * kD + G + hb + r] = lsum[r];
+      }
+  }
+  wave_lds_sync();
+
+  // P.V: acc[h][e] over this lane's 16 tokens, then across the 4 rows.
+  constexpr int HC = Cfg<G>::HC;
+#pragma unroll
+  for (int hc0 = 0; hc0 < G; hc0 += HC) {
+    float acc[HC][8];
+#pragma unroll
+    for (int h = 0; h < HC; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float* pp = pbuf + (16 * hi + i) * G + hc0;
+      float pv[HC];
+#pragma unroll
+      for (int h = 0; h < HC; ++h) pv[h] = pp[h];
+      const u32x4 w = vr[i];
+      float v[8];
+      v[0] = bf_lo(w[0]); v[1] = bf_hi(w[0]); v[2] = bf_lo(w[1]); v[3] = bf_hi(w[1]);
+      v[4] = bf_lo(w[2]); v[5] = bf_hi(w[2]); v[6] = bf_lo(w[3]); v[7] = bf_hi(w[3]);
+#pragma unroll
+      for (int h = 0; h < HC; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = __builtin_fmaf(pv[h], v[e], acc[h][e]);
+    }
+#pragma unroll
+    for (int h = 0; h < HC; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float x = acc[h][e];
+        x = x + __shfl_xor(x, 16);
+        x = x + __shfl_xor(x, 32);
+        acc[h][e] = x;
+      }
+#pragma unroll
+    for (int h = 0; h < HC; ++h) {
+      const int hg = hc0 + h;
+      const int owner = G >= 4 ? (hg & 3) : hg;
+      if (owner == hi) {
+        f32x4* dst = reinterpret_cast<f32x4*>(rec + hg * kD + lo * 8);
+        dst[0] = f32x4{acc[h][0], acc[h][1], acc[h][2], acc[h][3]};
+        dst[1] = f32x4{acc[h][4], acc[h][5], acc[h][6], acc[h][7]};
+      }
+    }
+  }
+}
+
+// ---- phase 2 helpers ----------------------------------------------------------
+struct StabSummary {   // one chunk's own blocks (entering run taken as 0)
+  int32_t lead;        // leading stable blocks
+  int32_t trail;       // trailing stable blocks
+  int32_t len;         // blocks in the chunk
+  int32_t fis;         // first block (0-based) where the chunk's own run reaches p, or -1
+};
+struct StabState {     // after a prefix of chunks
+  int32_t stopped;     // 1 if the stop lies in the prefix
+  int32_t stop_t;      // 1-based traversal step of the stop
+  int32_t run;         // consecutive stable steps ending the prefix (if not stopped)
+  int32_t pad;
+};
+
+__device__ __forceinline__ StabState stab_fold(StabState x, StabSummary y, int t0, int patience) {
+  if (x.stopped) return x;
+  StabState r = x;
+  if (y.lead > 0 && (int64_t)x.run + y.lead >= patience) {
+    r.stopped = 1;
+    r.stop_t = t0 + (patience - x.run - 1) + 1;
+  } else if (y.fis >= 0) {
+    r.stopped = 1;
+    r.stop_t = t0 + y.fis + 1;
+  } else {
+    r.run = (y.lead == y.len) ? x.run + y.len : y.trail;
+  }
+  return r;
+}
+
+// Spin until chunk j of group gidx reaches state >= need (returns it), or
+// until a stop in a chunk before `me` is announced / the spin limit is hit
+// (returns -1; on the limit the error word is set).
+__device__ int wait_state(const KernelParams& P, int gidx, int j, uint32_t need, int me) {
+  const uint64_t* f = P.flags + (int64_t)gidx * P.max_chunks + j;
+  for (uint32_t it = 0;; ++it) {
+    const uint32_t st = flag_state(ld_relaxed(f), P.epoch);
+    if (st >= need) return (int)st;
+    if (ld_relaxed(P.stop_epoch + gidx) == P.epoch) {
+      acquire_agent();
+      if ((int)ld_relaxed32(P.stop_chunk + gidx) < me) return -1;
+    }
+    if (it >= P.spin_limit) {
+      __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return -1;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+__device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, uint32_t state, int lane) {
+  release_agent();
+  if (lane == 0)
+    __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, (P.epoch << 3) | state,
+                       __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int G>
+__device__ void write_outputs(const KernelParams& P, int b, int kvh, const State<G>& s,
+                              int stop, int lane) {
+  const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    const int h = r + 4 * k;
+    if (h >= G) continue;
+    const int64_t row = (int64_t)b * P.num_q_heads + kvh * G + h;
+    if (P.out_bf16) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = f32_to_bf16_bits(s.o[k][2 * e]) | (f32_to_bf16_bits(s.o[k][2 * e + 1]) << 16);
+      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(P.out) + row * kD + c * 8) = u32x4{w[0], w[1], w[2], w[3]};
+    } else {
+      f32x4* dst = reinterpret_cast<f32x4*>(static_cast<float*>(P.out) + row * kD + c * 8);
+      dst[0] = f32x4{s.o[k][0], s.o[k][1], s.o[k][2], s.o[k][3]};
+      dst[1] = f32x4{s.o[k][4], s.o[k][5], s.o[k][6], s.o[k][7]};
+    }
+    if (c == 0) {
+      // natural log of sum exp(scale q.k): (m + log2 L) * ln 2
+      P.lse[row] = (s.m[k] + __log2f(s.L[k])) * 0.69314718055994531f;
+    }
+  }
+  if (lane == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = stop;
+}
+
+template <int G>
+__device__ void write_empty(const KernelParams& P, int b, int kvh) {
+  for (int i = threadIdx.x; i < G * kD; i += kThreads) {
+    const int64_t idx = ((int64_t)b * P.num_q_heads + kvh * G) * kD + i;
+    if (P.out_bf16) static_cast<uint16_t*>(P.out)[idx] = 0;
+    else static_cast<float*>(P.out)[idx] = 0.f;
+  }
+  if ((int)threadIdx.x < G) P.lse[(int64_t)b * P.num_q_heads + kvh * G + threadIdx.x] = kNegInf;
+  if (threadIdx.x == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = 0;
+}
+
+// ---- the kernel -----------------------------------------------------------------
+template <int G>
+__global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
+  extern __shared__ float smem[];
+  __shared__ int s_claim;
+  __shared__ int s_exit;
+  constexpr int REC = Cfg<G>::REC;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int n_groups = P.batch * P.num_kv_heads;
+  const int gidx = blockIdx.x % n_groups;
+  const int khint = blockIdx.x / n_groups;
+  const int b = gidx / P.num_kv_heads, kvh = gidx - b * P.num_kv_heads;
+
+  // traversal length (indices are clamped: malformed input never reads
+  // outside the arrays the shape describes)
+  const int64_t cap = (int64_t)P.max_pages << P.page_shift;
+  int L = P.seq_lens[b];
+  L = L < 0 ? 0 : (int)min((int64_t)L, cap);
+  const int Bk = P.block_size;
+  const int nblk = (L + Bk - 1) / Bk;
+  const int32_t* list = nullptr;
+  int T = nblk;
+  if (P.block_list) {
+    const int row = P.list_per_head ? gidx : b;
+    T = P.block_list_len[row];
+    T = T < 0 ? 0 : min(T, P.max_list);
+    list = P.block_list + (int64_t)row * P.max_list;
+  }
+  if (nblk == 0) T = 0;
+  T = min(T, P.t_cap);
+  const int C = P.chunk_blocks;
+  const int n_chunks = (T + C - 1) / C;
+  if (n_chunks == 0) {
+    if (khint == 0) write_empty<G>(P, b, kvh);
+    return;
+  }
+  if (khint >= n_chunks) return;
+
+  if (tid == 0) {
+    const uint32_t k = __hip_atomic_fetch_add(P.claim + gidx, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((int)k == n_chunks - 1)  // last claim of this call: reset for the next call
+      __hip_atomic_store(P.claim + gidx, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int ex = 0;
+    if (ld_relaxed(P.stop_epoch + gidx) == P.epoch) {
+      acquire_agent();
+      ex = (int)ld_relaxed32(P.stop_chunk + gidx) < (int)k;
+    }
+    s_claim = (int)k;
+    s_exit = ex;
+  }
+  __syncthreads();
+  const int k = s_claim;
+  if (s_exit) return;
+  if (k >= n_chunks) {  // the workspace was not zero-filled: refuse rather than index past it
+    if (tid == 0) __hip_atomic_store(P.error_word, 7u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+
+  const int t0 = k * C;                 // first traversal step (0-based) of the chunk
+  const int nb = min(C, T - t0);
+  const int tpb = P.tiles_per_block;
+  const int ntiles = nb * tpb;
+  float* tiles = smem;
+  float* pbuf = smem + P.chunk_tiles_lds * REC + wave * (kTile * G);
+
+  {
+    bf16x8 qa[4];
+    load_q<G>(P, b, kvh, lane, qa);
+    for (int ti = wave; ti < ntiles; ti += kWaves) {
+      const int i = ti / tpb, j = ti - i * tpb;
+      const int step = t0 + i;
+      int blk;
+      if (list) {
+        blk = list[step];
+        blk = blk < 0 ? 0 : (blk >= nblk ? nblk - 1 : blk);
+      } else {
+        blk = P.dense_order == 1 ? step : nblk - 1 - step;
+      }
+      compute_tile<G>(P, b, kvh, L, blk * Bk + j * kTile, qa, pbuf, tiles + ti * REC);
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;
+
+  // ---------------- phase 2: wave 0 ----------------
+  float* rec_agg = P.records + ((int64_t)gidx * P.max_chunks + k) * 2 * P.record_floats;
+  float* rec_inc = rec_agg + P.record_floats;
+
+  // chunk aggregate: left fold over blocks, each block a left fold over tiles
+  State<G> agg;
+  state_clear<G>(agg);
+  for (int i = 0; i < nb; ++i) {
+    State<G> blkst, t;
+    state_clear<G>(blkst);
+    for (int j = 0; j < tpb; ++j) {
+      read_tile<G>(tiles + (i * tpb + j) * REC, t, lane);
+      merge<G, false>(blkst, t);
+    }
+    merge<G, false>(agg, blkst);
+  }
+  write_state<G>(rec_agg, agg, lane);
+  publish(P, gidx, k, kAggregate, lane);
+
+  // softmax look-back: nearest chunk with an inclusive state, then fold forward
+  int j = k - 1;
+  while (j >= 0) {
+    const int st = wait_state(P, gidx, j, kAggregate, k);
+    if (st < 0) return;
+    if (st >= (int)kInclusive) break;
+    --j;
+  }
+  acquire_agent();
+  State<G> pre;
+  if (j >= 0) {
+    read_state<G>(P.records + ((int64_t)gidx * P.max_chunks + j) * 2 * P.record_floats + P.record_floats, pre, lane);
+  } else {
+    state_clear<G>(pre);
+  }
+  for (int i = j + 1; i < k; ++i) {
+    State<G> a;
+    read_state<G>(P.records + ((int64_t)gidx * P.max_chunks + i) * 2 * P.record_floats, a, lane);
+    merge<G, false>(pre, a);
+  }
+  {
+    State<G> inc = pre;
+    merge<G, false>(inc, agg);
+    write_state<G>(rec_inc, inc, lane);
+    publish(P, gidx, k, kInclusive, lane);
+  }
+
+  // replay the chunk's blocks from the prefix with the stability test
+  uint32_t stable_bits = 0;
+  {
+    State<G> s = pre;
+    for (int i = 0; i < nb; ++i) {
+      State<G> blkst, t;
+      state_clear<G>(blkst);
+      for (int jj = 0; jj < tpb; ++jj) {
+        read_tile<G>(tiles + (i * tpb + jj) * REC, t, lane);
+        merge<G, false>(blkst, t);
+      }
+      float old_o[Cfg<G>::HPL][8];
+#pragma unroll
+      for (int kk = 0; kk < Cfg<G>::HPL; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) old_o[kk][e] = s.o[kk][e];
+      float d[Cfg<G>::HPL][8];
+      merge<G, true>(s, blkst, d);
+      bool ok = true;
+#pragma unroll
+      for (int kk = 0; kk < Cfg<G>::HPL; ++kk) {
+        float n0 = 0.f, dd = 0.f, od = 0.f, n1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          n0 = __builtin_fmaf(old_o[kk][e], old_o[kk][e], n0);
+          dd = __builtin_fmaf(d[kk][e], d[kk][e], dd);
+          od = __builtin_fmaf(old_o[kk][e], d[kk][e], od);
+          n1 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n1);
+        }
+        n0 = row_sum(n0);
+        dd = row_sum(dd);
+        od = row_sum(od);
+        n1 = row_sum(n1);
+        // Eq. (2): d_scale = |d|; d_direction = 1 - cos(o_new, o_old)
+        const float d_scale = __fsqrt_rn(dd);
+        const float nn = __fmul_rn(__fsqrt_rn(n1), __fsqrt_rn(n0));
+        const float dot = __fadd_rn(n0, od);
+        float d_dir;
+        if (dot > 0.f) {
+          const float num = fmaxf(__fsub_rn(__fmul_rn(n0, dd), __fmul_rn(od, od)), 0.f);
+          d_dir = __fdiv_rn(num, __fmul_rn(nn, __fadd_rn(nn, dot)));
+        } else {
+          d_dir = __fsub_rn(1.f, __fdiv_rn(dot, nn));
+        }
+        const bool st = (n0 > 0.f) && (n1 > 0.f) && (d_scale < P.tau) && (d_dir < P.phi);
+        if (slot_valid<G>(lane, kk) && !st) ok = false;
+      }
+      const bool all_ok = __all(ok);
+      stable_bits |= (all_ok ? 1u : 0u) << i;
+      write_state<G>(tiles + i * tpb * REC, s, lane);   // o(t) after block i, for the output
+    }
+  }
+
+  // stability summary of this chunk (entering run 0)
+  StabSummary sm;
+  {
+    int run = 0, lead = 0, fis = -1;
+    bool leading = true;
+    for (int i = 0; i < nb; ++i) {
+      const bool st = (stable_bits >> i) & 1u;
+      run = st ? run + 1 : 0;
+      if (leading) {
+        if (st) ++lead;
+        else leading = false;
+      }
+      if (fis < 0 && run >= P.patience) fis = i;
+    }
+    sm.lead = lead;
+    sm.trail = run;
+    sm.len = nb;
+    sm.fis = fis;
+  }
+  int32_t* stab_me = P.stab + ((int64_t)gidx * P.max_chunks + k) * 8;
+  if (lane == 0) {
+    stab_me[0] = sm.lead;
+    stab_me[1] = sm.trail;
+    stab_me[2] = sm.len;
+    stab_me[3] = sm.fis;
+  }
+  publish(P, gidx, k, kStabSummary, lane);
+
+  // stability look-back
+  j = k - 1;
+  while (j >= 0) {
+    const int st = wait_state(P, gidx, j, kStabSummary, k);
+    if (st < 0) return;
+    if (st >= (int)kStabInclusive) break;
+    --j;
+  }
+  acquire_agent();
+  StabState x{0, 0, 0, 0};
+  if (j >= 0) {
+    const int32_t* sj = P.stab + ((int64_t)gidx * P.max_chunks + j) * 8;
+    x.stopped = sj[4];
+    x.stop_t = sj[5];
+    x.run = sj[6];
+  }
+  for (int i = j + 1; i < k; ++i) {
+    const int32_t* si = P.stab + ((int64_t)gidx * P.max_chunks + i) * 8;
+    StabSummary y{si[0], si[1], si[2], si[3]};
+    x = stab_fold(x, y, i * C, P.patience);
+  }
+  const bool stopped_before = x.stopped != 0;
+  const StabState y = stab_fold(x, sm, t0, P.patience);
+  if (lane == 0) {
+    stab_me[4] = y.stopped;
+    stab_me[5] = y.stop_t;
+    stab_me[6] = y.run;
+  }
+  if (!stopped_before && y.stopped) {
+    // the stop lies in this chunk: write o(t*) and announce the stop
+    State<G> s;
+    read_state<G>(tiles + (y.stop_t - 1 - t0) * tpb * REC, s, lane);
+    write_outputs<G>(P, b, kvh, s, y.stop_t, lane);
+    if (lane == 0) {
+      __hip_atomic_store(P.stop_chunk + gidx, (uint32_t)k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    release_agent();
+    if (lane == 0)
+      __hip_atomic_store(P.stop_epoch + gidx, P.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  } else if (!y.stopped && k == n_chunks - 1) {
+    State<G> s;
+    read_state<G>(tiles + (nb - 1) * tpb * REC, s, lane);
+    write_outputs<G>(P, b, kvh, s, T, lane);
+  }
+  publish(P, gidx, k, kStabInclusive, lane);
+}
+
+__global__ void fill_zero_kernel(uint32_t* p, size_t n_words) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_words; i += stride) p[i] = 0u;
+}
+
+template <int G>
+int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
+  const int64_t grid = (int64_t)plan.n_groups * plan.max_chunks;
+  if (grid <= 0) return (int)hipSuccess;
+  hipLaunchKernelGGL(art_decode_kernel<G>, dim3((unsigned)grid), dim3(kThreads),
+                     plan.lds_bytes, stream, params);
+  return (int)hipGetLastError();
+}
+
+}  // namespace
+
+int launch_decode(const Plan& plan, const KernelParams& params, hipStream_t stream) {
+  switch (plan.group) {
+    case 1: return launch_g<1>(plan, params, stream);
+    case 2: return launch_g<2>(plan, params, stream);
+    case 4: return launch_g<4>(plan, params, stream);
+    case 8: return launch_g<8>(plan, params, stream);
+    case 16: return launch_g<16>(plan, params, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+int launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream) {
+  const size_t words = bytes / 4;
+  if (words == 0) return (int)hipSuccess;
+  size_t blocks = (words + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     static_cast<uint32_t*>(ptr), words);
+  return (int)hipGetLastError();
+}
+
+}  // namespace art

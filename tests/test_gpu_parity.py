@@ -1,0 +1,257 @@
+"""HIP path vs the CPU oracle, on the same seeded inputs (needs a gfx950 GPU).
+
+Every call goes through the C ABI (paper_2606_00024_amd.api ->
+libart.so).  Acceptance (tests/parity.py): stop_block bit-exact except
+reported near-ties, out within 2e-3 relative L2 per head, lse within 1e-4.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import random_lists, small_workload
+from parity import Report, compare_sampled, compare_workload
+from paper_2606_00024_amd import _lib, api, workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    _lib.load()  # fails loudly when the library is missing
+    yield
+
+
+def _run(wl, tau, phi, p, **kw):
+    _say(f"  gpu call: {wl.spec.name} B={wl.spec.batch} Hq={wl.spec.num_q_heads} "
+         f"Hkv={wl.spec.num_kv_heads} Bk={wl.spec.block_size} Ps={wl.spec.page_size} "
+         f"lens={wl.seq_lens.tolist()[:4]} list={wl.block_list is not None} "
+         f"tau={tau} phi={phi} p={p} {kw}")
+    r = api.decode_workload(wl, tau=tau, phi=phi, patience=p, **kw)
+    torch.cuda.synchronize()
+    return r
+
+
+def _to_dev(wl):
+    wl.q = wl.q.to(DEV)
+    wl.k_cache = wl.k_cache.to(DEV)
+    wl.v_cache = wl.v_cache.to(DEV)
+    wl.page_table = wl.page_table.to(DEV)
+    wl.seq_lens = wl.seq_lens.to(DEV)
+    if wl.block_list is not None:
+        wl.block_list = wl.block_list.to(DEV)
+        wl.block_list_len = wl.block_list_len.to(DEV)
+    return wl
+
+
+THRESHOLDS = [(1e-3, 1e-4, 5), (0.05, 1e-3, 2), (0.0, 1e-4, 5), (math.inf, 2e-3, 3), (0.02, math.inf, 1)]
+
+SMALL = [
+    # seed, B, Hkv, g, seq_len(s), Bk, Ps, order, lists
+    (1, 1, 2, 4, 4096, 64, 64, 0, False),
+    (2, 2, 2, 1, (700, 1500), 64, 16, 0, False),
+    (3, 1, 2, 2, 1500, 128, 64, 1, False),
+    (4, 2, 2, 8, (900, 2049), 64, 128, 0, True),
+    (5, 1, 1, 4, 64, 64, 64, 0, False),
+    (6, 1, 2, 16, 3000, 64, 32, 0, False),
+    (7, 3, 1, 4, (1, 65, 640), 64, 16, 0, False),
+    (8, 1, 4, 4, 5000, 256, 256, 0, False),
+    (9, 2, 2, 4, (3000, 777), 128, 16, 0, True),
+]
+
+
+def _small(case):
+    seed, B, hkv, g, L, bk, ps, order, lists = case
+    wl = small_workload(seed, batch=B, kv_heads=hkv, group=g, seq_len=L, block_size=bk,
+                        page_size=ps, dense_order=order, needles=2)
+    if lists:
+        wl.block_list, wl.block_list_len = random_lists(wl, seed, fraction=0.6)
+    return _to_dev(wl)
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[f"s{c[0]}" for c in SMALL])
+@pytest.mark.parametrize("thr", THRESHOLDS, ids=["cfg", "relaxed", "off", "dir_only", "scale_only_p1"])
+def test_small_matrix(case, thr):
+    wl = _small(case)
+    tau, phi, p = thr
+    gpu = _run(wl, tau, phi, p)
+    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p)
+    _say("  ", rep)
+    assert rep.ok(), str(rep)
+
+
+@pytest.mark.parametrize("chunk", [1, 2, 3, 5, 16])
+def test_chunking_changes_rounding_only(chunk):
+    wl = _small((11, 2, 2, 4, (3000, 2500), 64, 64, 0, False))
+    for thr in [(1e-3, 1e-4, 5), (0.05, 1e-3, 2), (0.0, 1e-4, 5)]:
+        gpu = _run(wl, *thr, chunk_blocks=chunk)
+        rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2])
+        _say("  ", chunk, thr, rep)
+        assert rep.ok(), str(rep)
+
+
+def test_bf16_output():
+    wl = _small((12, 1, 2, 4, 2000, 64, 64, 0, False))
+    out, lse, stop = _run(wl, 1e-3, 1e-4, 5, out_dtype=torch.bfloat16)
+    assert out.dtype == torch.bfloat16
+    f32 = _run(wl, 1e-3, 1e-4, 5)
+    assert torch.equal(stop, f32[2]) and torch.equal(lse, f32[1])
+    assert torch.equal(out, f32[0].to(torch.bfloat16))  # round-to-nearest-even of the same fp32
+
+
+def test_deterministic_repeats():
+    wl = _small((13, 2, 2, 4, (4000, 3333), 64, 64, 0, False))
+    for thr in [(1e-3, 1e-4, 5), (0.0, 1e-4, 5)]:
+        first = _run(wl, *thr, chunk_blocks=1)
+        for _ in range(20):
+            again = api.decode_workload(wl, tau=thr[0], phi=thr[1], patience=thr[2], chunk_blocks=1)
+            for a, b in zip(first, again):
+                assert torch.equal(a, b)
+    torch.cuda.synchronize()
+
+
+def test_monotone_thresholds_on_gpu():
+    wl = _small((14, 2, 2, 4, (4096, 3000), 64, 64, 0, False))
+    base = _run(wl, 0.05, 1e-3, 2)[2]
+    for tau, phi, p in [(0.05, 1e-3, 3), (0.02, 1e-3, 2), (0.05, 1e-4, 2), (0.01, 1e-4, 6)]:
+        tighter = _run(wl, tau, phi, p)[2]
+        assert (tighter >= base).all()
+
+
+def test_empty_inputs_and_shared_lists():
+    wl = small_workload(15, batch=3, kv_heads=2, group=4, seq_len=(0, 1000, 64), needles=2)
+    _to_dev(wl)
+    gpu = _run(wl, 1e-3, 1e-4, 5)
+    rep = compare_workload(wl, gpu, tau=1e-3, phi=1e-4, patience=5)
+    assert rep.ok(), str(rep)
+    assert gpu[2][0].tolist() == [0, 0]
+    # one list per sequence shared by its KV heads; one empty list
+    bl, bll = random_lists(wl, 15, fraction=0.5)
+    shared = bl[:, 0, :].contiguous().to(DEV)
+    shared_len = bll[:, 0].contiguous().to(DEV)
+    shared_len[2] = 0
+    _say("  gpu call: shared lists")
+    out, lse, stop = api.decode_attention(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens,
+                                          block_size=64, tau=1e-3, phi=1e-4, patience=5,
+                                          block_list=shared, block_list_len=shared_len,
+                                          list_per_head=False)
+    torch.cuda.synchronize()
+    ref = oracle.decode(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens, block_size=64,
+                        scale=1 / math.sqrt(128), tau=1e-3, phi=1e-4, patience=5,
+                        block_list=shared.cpu(), block_list_len=shared_len.cpu(),
+                        list_per_head=False)
+    assert np.array_equal(stop.cpu().numpy(), ref["stop"])
+    o = out.double().cpu().numpy()
+    mask = ref["stop"].repeat(4, axis=1) > 0
+    err = np.linalg.norm(o - ref["out"], axis=-1)[mask] / np.linalg.norm(ref["out"], axis=-1)[mask]
+    assert err.max() <= 2e-3
+    assert np.all(o[~mask] == 0)
+
+
+def test_validate_inputs_flags_bad_indices():
+    wl = _small((16, 2, 2, 4, (1000, 600), 64, 64, 0, True))
+    s = wl.spec
+    st, idx, where = api.validate_inputs(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens,
+                                         block_size=64, block_list=wl.block_list,
+                                         block_list_len=wl.block_list_len)
+    assert st == _lib.OK
+    bad = wl.block_list.clone()
+    bad[1, 1, 0] = 99
+    st, idx, where = api.validate_inputs(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens,
+                                         block_size=64, block_list=bad, block_list_len=wl.block_list_len)
+    assert (st, where) == (_lib.ERR_BAD_INDEX, 2) and idx == (1 * 2 + 1) * bad.shape[2]
+    dup = wl.block_list.clone()
+    dup[0, 0, 1] = dup[0, 0, 0]
+    st, idx, where = api.validate_inputs(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens,
+                                         block_size=64, block_list=dup, block_list_len=wl.block_list_len)
+    assert (st, where, idx) == (_lib.ERR_BAD_INDEX, 2, 1)
+    pt = wl.page_table.clone()
+    pt[1, 3] = 10 ** 6
+    st, idx, where = api.validate_inputs(wl.q, wl.k_cache, wl.v_cache, pt, wl.seq_lens, block_size=64)
+    assert (st, where, idx) == (_lib.ERR_BAD_INDEX, 1, pt.shape[1] + 3)
+    sl = wl.seq_lens.clone()
+    sl[0] = -5
+    st, idx, where = api.validate_inputs(wl.q, wl.k_cache, wl.v_cache, wl.page_table, sl, block_size=64)
+    assert (st, where, idx) == (_lib.ERR_BAD_INDEX, 0, 0)
+
+
+def test_malformed_indices_stay_in_bounds():
+    """Out-of-range ids are clamped on the device: the call completes and
+    every output is finite (the values themselves are unspecified)."""
+    wl = small_workload(17, batch=1, kv_heads=2, group=4, seq_len=1000, needles=2, nan_fill=False)
+    wl.block_list, wl.block_list_len = random_lists(wl, 17, fraction=0.6)
+    _to_dev(wl)
+    bl = wl.block_list.clone()
+    bl[0, 0, :] = 10 ** 6
+    bl[0, 1, 0] = -7
+    pt = wl.page_table.clone()
+    pt[0, 2] = -1
+    pt[0, 3] = 10 ** 7
+    _say("  gpu call: clamped indices")
+    ws = api.new_workspace(1 << 22, DEV)
+    out, lse, stop = api.decode_attention(wl.q, wl.k_cache, wl.v_cache, pt, wl.seq_lens,
+                                          block_size=64, tau=1e-3, phi=1e-4, patience=5,
+                                          block_list=bl, block_list_len=wl.block_list_len,
+                                          workspace=ws)
+    torch.cuda.synchronize()
+    assert api.workspace_status(ws) == _lib.OK
+    assert torch.isfinite(lse).all() and (stop >= 1).all()
+
+
+def test_workspace_reuse_across_shapes():
+    ws = api.new_workspace(64 << 20, DEV)
+    for case in [SMALL[0], SMALL[3], SMALL[5], SMALL[0]]:
+        wl = _small(case)
+        gpu = _run(wl, 1e-3, 1e-4, 5, workspace=ws)
+        rep = compare_workload(wl, gpu, tau=1e-3, phi=1e-4, patience=5)
+        assert rep.ok(), str(rep)
+    assert api.workspace_status(ws) == _lib.OK
+
+
+# ------------------------------------------------------------ full-size workloads
+
+def _sample_groups(wl, n, seed):
+    s = wl.spec
+    rng = np.random.default_rng(seed)
+    all_g = [(b, h) for b in range(s.batch) for h in range(s.num_kv_heads)]
+    idx = rng.choice(len(all_g), size=min(n, len(all_g)), replace=False)
+    return sorted(all_g[i] for i in idx)
+
+
+FULL = [("tiny_4k", 2), ("llama3_8b_32k", 6), ("sparse25_128k", 6), ("qwen3_32b_ragged", 6),
+        ("long_512k", 3)]
+
+
+@pytest.mark.parametrize("name,nsample", FULL, ids=[f[0] for f in FULL])
+def test_full_size(name, nsample):
+    spec = W.WORKLOADS[name]
+    _say(f"  generating {name} on {DEV}")
+    wl = W.make_workload(spec, device=DEV)
+    torch.cuda.synchronize()
+    groups = _sample_groups(wl, nsample, spec.seed)
+    modes = [(spec.tau, spec.phi, spec.patience), (0.0, spec.phi, spec.patience)]
+    if name == "qwen3_32b_ragged":
+        modes = [(t, f, spec.patience) for t, f in W.RAGGED_SWEEP] + [(0.0, 1e-4, 5)]
+    for tau, phi, p in modes:
+        gpu = _run(wl, tau, phi, p)
+        rep = compare_sampled(wl, gpu, groups, tau=tau, phi=phi, patience=p)
+        skipped = 1 - gpu[2].sum().item() / sum(map(sum, wl.traversal_lengths()))
+        _say(f"   {name} tau={tau} phi={phi}: {rep}  skipped={skipped:.3f}")
+        assert rep.ok(), str(rep)
+    del wl
+    torch.cuda.empty_cache()
