@@ -75,20 +75,28 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     if (t_cap > INT32_MAX / 2) return ART_ERR_UNSUPPORTED;
     const int64_t n_groups = (int64_t)s->batch * s->num_kv_heads;
 
-    const int rec_tile = g * art::kHeadDim + 2 * g;                 // floats
-    const size_t pbuf_bytes = (size_t)art::kWaves * art::kTile * g * 4;
+    // LDS of a workgroup: two chunk buffers of C*tpb tile records plus three
+    // per-loader partial aggregates each (when they fit), and three P.V
+    // staging buffers.  Kept within 64 KiB.
+    const size_t rec_bytes = (size_t)(g * art::kHeadDim + 2 * g) * 4;
+    const size_t pbuf_bytes = (size_t)3 * art::kTile * g * 4;
     const size_t lds_cap = 64 * 1024;
+    auto lds_for = [&](int tiles, int partials) {
+        return 2 * (size_t)(tiles + partials) * rec_bytes + pbuf_bytes;
+    };
+    int partials = 3;
+    if (lds_for(tpb, partials) > lds_cap) partials = 0;
+    if (lds_for(tpb, partials) > lds_cap) return ART_ERR_UNSUPPORTED;
     int max_tiles = art::kMaxChunkTiles;
-    while (max_tiles > tpb && (size_t)max_tiles * rec_tile * 4 + pbuf_bytes > lds_cap) --max_tiles;
-    if ((size_t)tpb * rec_tile * 4 + pbuf_bytes > lds_cap) return ART_ERR_UNSUPPORTED;
+    while (max_tiles > tpb && lds_for(max_tiles, partials) > lds_cap) --max_tiles;
     const int c_max = max_tiles / tpb;
 
     int C;
     if (o->chunk_blocks > 0) {
         C = o->chunk_blocks;
     } else {
-        // about 8 tiles (two per wavefront) per chunk; smaller chunks when
-        // the whole problem would not give the 256 CUs enough workgroups
+        // about 8 tiles per chunk; smaller chunks when the whole problem
+        // would not give the 256 CUs enough work
         C = 8 / tpb;
         if (C < 1) C = 1;
         while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
@@ -105,7 +113,8 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     p->n_groups = (int32_t)n_groups;
     p->t_cap = (int32_t)t_cap;
     p->record_floats = (g * art::kHeadDim + 2 * g + 63) / 64 * 64;
-    p->lds_bytes = (size_t)C * tpb * rec_tile * 4 + pbuf_bytes;
+    p->loader_partials = partials;
+    p->lds_bytes = lds_for(C * tpb, partials);
 
     art::WorkspaceLayout& w = p->ws;
     size_t off = 0;
@@ -113,9 +122,12 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     w.claim_off = off;      off = align_up(off + 4 * (size_t)n_groups);
     w.stop_epoch_off = off; off = align_up(off + 8 * (size_t)n_groups);
     w.stop_chunk_off = off; off = align_up(off + 4 * (size_t)n_groups);
+    w.resolved_off = off;   off = align_up(off + 8 * (size_t)n_groups);
     w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
     w.stab_off = off;       off = align_up(off + 32 * (size_t)n_groups * max_chunks);
     w.records_off = off;    off = align_up(off + (size_t)n_groups * max_chunks * 2 * p->record_floats * 4);
+    // one group's records are addressed with 32-bit byte offsets
+    if ((int64_t)max_chunks * 2 * p->record_floats * 4 > INT32_MAX) return ART_ERR_UNSUPPORTED;
     w.total = off;
     return ART_OK;
 }
@@ -201,6 +213,7 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.t_cap = plan.t_cap;
     k.record_floats = plan.record_floats;
     k.chunk_tiles_lds = plan.chunk_blocks * plan.tiles_per_block;
+    k.loader_partials = plan.loader_partials;
     k.q = static_cast<const uint16_t*>(q);
     k.k = static_cast<const uint16_t*>(k_cache);
     k.v = static_cast<const uint16_t*>(v_cache);
@@ -216,12 +229,13 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.claim = reinterpret_cast<uint32_t*>(ws + plan.ws.claim_off);
     k.stop_epoch = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_epoch_off);
     k.stop_chunk = reinterpret_cast<uint32_t*>(ws + plan.ws.stop_chunk_off);
+    k.resolved = reinterpret_cast<uint64_t*>(ws + plan.ws.resolved_off);
     k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
     k.stab = reinterpret_cast<int32_t*>(ws + plan.ws.stab_off);
     k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
     k.epoch = g_epoch.fetch_add(1, std::memory_order_relaxed) + 1;
     k.spin_limit = kSpinLimit;
-    if (k.epoch >= (uint64_t(1) << 60)) return ART_ERR_UNSUPPORTED;
+    if (k.epoch >= (uint64_t(1) << 40)) return ART_ERR_UNSUPPORTED;
     return art::launch_decode(plan, k, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
 }
 

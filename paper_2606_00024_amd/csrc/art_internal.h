@@ -31,6 +31,7 @@ struct WorkspaceLayout {
     size_t claim_off;        // uint32 [groups] chunk-claim counters
     size_t stop_epoch_off;   // uint64 [groups] epoch of the announced stop
     size_t stop_chunk_off;   // uint32 [groups] chunk that holds the stop
+    size_t resolved_off;     // uint64 [groups] epoch << 24 | resolved chunks
     size_t flags_off;        // uint64 [groups][max_chunks]
     size_t stab_off;         // int32 [groups][max_chunks][8]
     size_t records_off;      // float [groups][max_chunks][2][record_floats]
@@ -45,6 +46,7 @@ struct Plan {
     int32_t n_groups;        // batch * num_kv_heads
     int32_t t_cap;           // traversal length bound per group
     int32_t record_floats;   // floats per aggregate / inclusive record
+    int32_t loader_partials; // see KernelParams
     size_t lds_bytes;        // dynamic LDS per workgroup
     WorkspaceLayout ws;
 };
@@ -61,7 +63,8 @@ struct KernelParams {
     int32_t patience, dense_order, out_bf16;
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
-    int32_t chunk_tiles_lds; // tile records that fit in dynamic LDS
+    int32_t chunk_tiles_lds; // tile records per LDS chunk buffer
+    int32_t loader_partials; // per-loader partial aggregates kept in LDS (3 or 0)
     // data
     const uint16_t* q;
     const uint16_t* k;
@@ -78,6 +81,7 @@ struct KernelParams {
     uint32_t* claim;
     uint64_t* stop_epoch;
     uint32_t* stop_chunk;
+    uint64_t* resolved;
     uint64_t* flags;
     int32_t* stab;
     float* records;

@@ -15,7 +15,10 @@
 //   only ever waits on chunks that are already running: no deadlock whatever
 //   the dispatch order.
 //
-//   Phase 1 (all 4 waves): each wave streams 64-token tiles of the chunk's
+//   A chunk starts loading only within a window of chunks past the group's
+//   resolved frontier, which bounds the reads wasted past a stop.
+//
+//   Phase 1 (all 4 wavefronts): each streams 64-token tiles of the chunk's
 //   blocks from HBM (16-byte loads, four 64-byte row segments per K load
 //   instruction, four 256-byte rows per V load instruction), computes the
 //   scores of all g query heads with v_mfma_f32_16x16x32_bf16 (query heads
@@ -23,7 +26,7 @@
 //   softmax in base 2 with row reductions over DPP, and P.V on the VALU in
 //   fp32, and leaves (m, l, sum p v) for its tile in LDS.
 //
-//   Phase 2 (wave 0 only; the other waves retire):
+//   Phase 2 (wavefront 0; the other three retire):
 //     - folds the tiles into block partials and the chunk aggregate and
 //       publishes the aggregate;
 //     - obtains the softmax state after the previous chunk by looking back
@@ -40,8 +43,9 @@
 //       either stops inside the chunk (writes out/lse/stop_block and
 //       announces the stop so that later chunks skip their loads), or, as
 //       the last chunk, writes the untruncated result.
-//   Cross-workgroup data goes through the workspace with agent-scope
-//   release/acquire, as the XCDs of MI355X have separate L2 caches.
+//   Cross-workgroup data goes through the workspace with agent-coherent
+//   accesses only, as the XCDs of MI355X have separate L2 caches (see the
+//   workspace helpers below).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -105,16 +109,53 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+// single hardware instructions (about 1 ulp): the same bits wherever used
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float fast_sqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
 
-// ---- workspace flags ---------------------------------------------------------
+// ---- workspace: cross-workgroup data ---------------------------------------
+// Everything one workgroup hands to another (flags, softmax records,
+// stability records, the stop announcement) is written and read only with
+// agent-scope atomic accesses, which gfx950 performs coherently across the
+// XCDs' L2 caches (sc1).  A writer waits for its data stores to complete
+// (s_waitcnt vmcnt(0)) before it stores the flag; a reader issues its data
+// loads only after the flag load has returned the expected value.  No L2
+// write-back or invalidate is needed, so publishing costs a few stores.
 __device__ __forceinline__ uint64_t ld_relaxed(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ uint32_t ld_relaxed32(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
-__device__ __forceinline__ void release_agent() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+__device__ __forceinline__ int32_t ld_coh_i32(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coh_i32(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coh_f32(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coh_f32(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// two adjacent floats through one 64-bit coherent access
+__device__ __forceinline__ void ld_coh_f32x2(const float* p, float& a, float& b) {
+  const uint64_t w = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  a = __uint_as_float((uint32_t)w);
+  b = __uint_as_float((uint32_t)(w >> 32));
+}
+__device__ __forceinline__ void st_coh_f32x2(float* p, float a, float b) {
+  const uint64_t w = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// wait until this wave's global stores have completed; also a compiler
+// barrier for memory operations
+__device__ __forceinline__ void stores_complete() {
+  __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
+}
+__device__ __forceinline__ void compiler_fence() { __asm__ __volatile__("" ::: "memory"); }
 
 __device__ __forceinline__ uint32_t flag_state(uint64_t v, uint64_t epoch) {
   return (v >> 3) == epoch ? (uint32_t)(v & 7u) : 0u;
@@ -169,7 +210,7 @@ __device__ __forceinline__ void merge(State<G>& s, const State<G>& p,
     const float a = v1 ? __fmul_rn(s.L[k], fast_exp2(__fsub_rn(s.m[k], mn))) : 0.f;
     const float bb = v2 ? __fmul_rn(p.L[k], fast_exp2(__fsub_rn(p.m[k], mn))) : 0.f;
     const float Ln = __fadd_rn(a, bb);
-    const float w = v2 ? (v1 ? __fdiv_rn(bb, Ln) : 1.f) : 0.f;
+    const float w = v2 ? (v1 ? __fmul_rn(bb, fast_rcp(Ln)) : 1.f) : 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float d = __fmul_rn(w, __fsub_rn(p.o[k][e], s.o[k][e]));
@@ -181,7 +222,8 @@ __device__ __forceinline__ void merge(State<G>& s, const State<G>& p,
   }
 }
 
-// ---- records: global (normalised state) and LDS tiles (unnormalised) ------
+// ---- records: workspace (coherent, normalised) and LDS tiles --------------
+// Record layout: o[G][128] | m[G] | L[G].
 template <int G>
 __device__ __forceinline__ void write_state(float* rec, const State<G>& s, int lane) {
   const int c = lane & 15, r = lane >> 4;
@@ -216,13 +258,60 @@ __device__ __forceinline__ void read_state(const float* rec, State<G>& s, int la
   }
 }
 
+// Workspace records go through a buffer resource over the group's record
+// area with the sc1 cache policy: agent-coherent 16-byte accesses whose
+// completion the compiler tracks like any other load or store.
+constexpr int kCoherent = 16;  // buffer cache policy: sc1
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t record_rsrc(const KernelParams& P, int gidx) {
+  const float* base = P.records + (int64_t)gidx * P.max_chunks * 2 * P.record_floats;
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0,
+                                           P.max_chunks * 2 * P.record_floats * 4, 0x00020000);
+}
+
+template <int G>
+__device__ __forceinline__ void publish_state(__amdgpu_buffer_rsrc_t rs, int rec_off, const State<G>& s,
+                                              int lane) {
+  const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    const int h = r + 4 * k;
+    if (h < G) {
+      const int off = (rec_off + h * kD + c * 8) * 4;
+      __builtin_amdgcn_raw_buffer_store_b128(f32x4{s.o[k][0], s.o[k][1], s.o[k][2], s.o[k][3]}, rs, off, 0, kCoherent);
+      __builtin_amdgcn_raw_buffer_store_b128(f32x4{s.o[k][4], s.o[k][5], s.o[k][6], s.o[k][7]}, rs, off + 16, 0, kCoherent);
+      if (c == 0) {
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s.m[k]), rs, (rec_off + G * kD + h) * 4, 0, kCoherent);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s.L[k]), rs, (rec_off + G * kD + G + h) * 4, 0, kCoherent);
+      }
+    }
+  }
+}
+
+template <int G>
+__device__ __forceinline__ void fetch_state(__amdgpu_buffer_rsrc_t rs, int rec_off, State<G>& s, int lane) {
+  const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+  for (int k = 0; k < Cfg<G>::HPL; ++k) {
+    int h = r + 4 * k;
+    if (h >= G) h = 0;
+    const int off = (rec_off + h * kD + c * 8) * 4;
+    const f32x4 x0 = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kCoherent);
+    const f32x4 x1 = __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, kCoherent);
+    s.o[k][0] = x0[0]; s.o[k][1] = x0[1]; s.o[k][2] = x0[2]; s.o[k][3] = x0[3];
+    s.o[k][4] = x1[0]; s.o[k][5] = x1[1]; s.o[k][6] = x1[2]; s.o[k][7] = x1[3];
+    s.m[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, (rec_off + G * kD + h) * 4, 0, kCoherent));
+    s.L[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, (rec_off + G * kD + G + h) * 4, 0, kCoherent));
+  }
+}
+
 // An LDS tile record holds sum p v (not normalised); normalise on read.
 template <int G>
 __device__ __forceinline__ void read_tile(const float* rec, State<G>& s, int lane) {
   read_state<G>(rec, s, lane);
 #pragma unroll
   for (int k = 0; k < Cfg<G>::HPL; ++k) {
-    const float inv = s.L[k] > 0.f ? __fdiv_rn(1.f, s.L[k]) : 0.f;
+    const float inv = s.L[k] > 0.f ? fast_rcp(s.L[k]) : 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) s.o[k][e] = __fmul_rn(s.o[k][e], inv);
   }
@@ -251,8 +340,9 @@ __device__ __forceinline__ int clamp_page(const KernelParams& P, int b, int tok)
 }
 
 // Writes into `rec` (LDS): sum_j p_hj v_j [G][128], m_h [G] (base 2), l_h [G].
+// pg[n] is the (uniform) physical page of the 16-token group n of the tile.
 template <int G>
-__device__ void compute_tile(const KernelParams& P, int b, int kvh, int L, int tok0,
+__device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, const int (&pg)[4],
                              const bf16x8 (&qa)[4], float* __restrict__ pbuf,
                              float* __restrict__ rec) {
   const int lane = threadIdx.x & 63;
@@ -275,27 +365,26 @@ __device__ void compute_tile(const KernelParams& P, int b, int kvh, int L, int t
   u32x4 kr[4][4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) {
-    const int gt = min(tok0 + 16 * n, L - 1);
-    const int pg = clamp_page(P, b, gt);
     const int tok = min(tok0 + 16 * n + lo, L - 1);
-    const uint16_t* kp = P.k + (int64_t)pg * P.ks_page + (int64_t)kvh * P.ks_head +
+    const uint16_t* kp = P.k + (int64_t)pg[n] * P.ks_page + (int64_t)kvh * P.ks_head +
                          (int64_t)(tok & psz_mask) * P.ks_tok;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
       kr[n][s] = *reinterpret_cast<const u32x4*>(kp + (4 * s + hi) * 8);
   }
-  // V: lane (lo, hi) holds tokens 16*hi + i, dims 8*lo .. +7.
+  // V: lane (lo, hi) holds tokens 16*hi + i, dims 8*lo .. +7.  Issued with
+  // the K loads so that one memory latency covers the whole tile.
   u32x4 vr[16];
   {
-    const int gt = min(tok0 + 16 * hi, L - 1);
-    const int pg = clamp_page(P, b, gt);
-    const uint16_t* vp = P.v + (int64_t)pg * P.vs_page + (int64_t)kvh * P.vs_head + lo * 8;
+    const int pgv = hi == 0 ? pg[0] : (hi == 1 ? pg[1] : (hi == 2 ? pg[2] : pg[3]));
+    const uint16_t* vp = P.v + (int64_t)pgv * P.vs_page + (int64_t)kvh * P.vs_head + lo * 8;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int tok = min(tok0 + 16 * hi + i, L - 1);
       vr[i] = *reinterpret_cast<const u32x4*>(vp + (int64_t)(tok & psz_mask) * P.vs_tok);
     }
   }
+  __builtin_amdgcn_sched_barrier(0);
 
   // Scores: S[n] = Q (16 head rows) x K^T (16 token columns), K = 128 dims.
   f32x4 S[4];
@@ -424,31 +513,50 @@ __device__ __forceinline__ StabState stab_fold(StabState x, StabSummary y, int t
   return r;
 }
 
-// Spin until chunk j of group gidx reaches state >= need (returns it), or
-// until a stop in a chunk before `me` is announced / the spin limit is hit
-// (returns -1; on the limit the error word is set).
-__device__ int wait_state(const KernelParams& P, int gidx, int j, uint32_t need, int me) {
-  const uint64_t* f = P.flags + (int64_t)gidx * P.max_chunks + j;
-  for (uint32_t it = 0;; ++it) {
-    const uint32_t st = flag_state(ld_relaxed(f), P.epoch);
-    if (st >= need) return (int)st;
-    if (ld_relaxed(P.stop_epoch + gidx) == P.epoch) {
-      acquire_agent();
-      if ((int)ld_relaxed32(P.stop_chunk + gidx) < me) return -1;
+__device__ __forceinline__ bool stop_announced_before(const KernelParams& P, int gidx, int me) {
+  if (ld_relaxed(P.stop_epoch + gidx) != P.epoch) return false;
+  compiler_fence();
+  return (int)ld_relaxed32(P.stop_chunk + gidx) < me;
+}
+
+// Look-back over the flags of chunks me-1, me-2, ... of group gidx, 64 per
+// poll (one per lane): returns the nearest chunk j whose state is >= need_hi
+// such that every chunk strictly between j and `me` has state >= need_lo,
+// -1 if all chunks 0..me-1 have state >= need_lo and none >= need_hi, or -2
+// when a stop in a chunk before `me` has been announced or the spin limit is
+// reached (the error word is set then).  Wave-uniform.
+__device__ int lookback_scan(const KernelParams& P, int gidx, int me, uint32_t need_lo,
+                             uint32_t need_hi, int lane) {
+  const uint64_t* flags = P.flags + (int64_t)gidx * P.max_chunks;
+  int hi = me - 1;
+  uint32_t it = 0;
+  while (hi >= 0) {
+    const int idx = hi - lane;
+    const uint32_t st = idx >= 0 ? flag_state(ld_relaxed(flags + idx), P.epoch) : 0u;
+    const uint64_t have_hi = __ballot(idx >= 0 && st >= need_hi);
+    const uint64_t have_lo = __ballot(idx < 0 || st >= need_lo);
+    const int first = have_hi ? __ffsll((unsigned long long)have_hi) - 1 : 64;
+    const uint64_t need = first >= 64 ? ~0ull : ((1ull << first) - 1ull);
+    if ((have_lo & need) == need) {
+      if (first < 64) return hi - first;
+      hi -= 64;  // 64 chunks with aggregates but no inclusive state: look further back
+      continue;
     }
-    if (it >= P.spin_limit) {
+    if (stop_announced_before(P, gidx, me)) return -2;
+    if (++it >= P.spin_limit) {
       __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return -1;
+      return -2;
     }
     __builtin_amdgcn_s_sleep(2);
   }
+  return -1;
 }
 
 __device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, uint32_t state, int lane) {
-  release_agent();
+  stores_complete();
   if (lane == 0)
     __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, (P.epoch << 3) | state,
-                       __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int G>
@@ -481,7 +589,7 @@ __device__ void write_outputs(const KernelParams& P, int b, int kvh, const State
 
 template <int G>
 __device__ void write_empty(const KernelParams& P, int b, int kvh) {
-  for (int i = threadIdx.x; i < G * kD; i += kThreads) {
+  for (int i = threadIdx.x; i < G * kD; i += blockDim.x) {
     const int64_t idx = ((int64_t)b * P.num_q_heads + kvh * G) * kD + i;
     if (P.out_bf16) static_cast<uint16_t*>(P.out)[idx] = 0;
     else static_cast<float*>(P.out)[idx] = 0.f;
@@ -490,134 +598,127 @@ __device__ void write_empty(const KernelParams& P, int b, int kvh) {
   if (threadIdx.x == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = 0;
 }
 
-// ---- the kernel -----------------------------------------------------------------
-template <int G>
-__global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
-  extern __shared__ float smem[];
-  __shared__ int s_claim;
-  __shared__ int s_exit;
-  constexpr int REC = Cfg<G>::REC;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int n_groups = P.batch * P.num_kv_heads;
-  const int gidx = blockIdx.x % n_groups;
-  const int khint = blockIdx.x / n_groups;
-  const int b = gidx / P.num_kv_heads, kvh = gidx - b * P.num_kv_heads;
+struct GroupInfo {
+  int b, kvh, L, nblk, T, n_chunks;
+  const int32_t* list;
+};
 
-  // traversal length (indices are clamped: malformed input never reads
-  // outside the arrays the shape describes)
+// Traversal of group gidx (indices are clamped: malformed input never makes
+// a kernel read outside the arrays the shape describes).
+__device__ __forceinline__ GroupInfo group_info(const KernelParams& P, int gidx) {
+  GroupInfo g;
+  g.b = gidx / P.num_kv_heads;
+  g.kvh = gidx - g.b * P.num_kv_heads;
   const int64_t cap = (int64_t)P.max_pages << P.page_shift;
-  int L = P.seq_lens[b];
+  int L = P.seq_lens[g.b];
   L = L < 0 ? 0 : (int)min((int64_t)L, cap);
-  const int Bk = P.block_size;
-  const int nblk = (L + Bk - 1) / Bk;
-  const int32_t* list = nullptr;
-  int T = nblk;
+  g.L = L;
+  g.nblk = (L + P.block_size - 1) / P.block_size;
+  g.list = nullptr;
+  int T = g.nblk;
   if (P.block_list) {
-    const int row = P.list_per_head ? gidx : b;
+    const int row = P.list_per_head ? gidx : g.b;
     T = P.block_list_len[row];
     T = T < 0 ? 0 : min(T, P.max_list);
-    list = P.block_list + (int64_t)row * P.max_list;
+    g.list = P.block_list + (int64_t)row * P.max_list;
   }
-  if (nblk == 0) T = 0;
-  T = min(T, P.t_cap);
+  if (g.nblk == 0) T = 0;
+  g.T = min(T, P.t_cap);
+  g.n_chunks = (g.T + P.chunk_blocks - 1) / P.chunk_blocks;
+  return g;
+}
+
+template <int G>
+__device__ void write_empty_wave(const KernelParams& P, int b, int kvh, int lane) {
+  for (int i = lane; i < G * kD; i += 64) {
+    const int64_t idx = ((int64_t)b * P.num_q_heads + kvh * G) * kD + i;
+    if (P.out_bf16) static_cast<uint16_t*>(P.out)[idx] = 0;
+    else static_cast<float*>(P.out)[idx] = 0.f;
+  }
+  if (lane < G) P.lse[(int64_t)b * P.num_q_heads + kvh * G + lane] = kNegInf;
+  if (lane == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = 0;
+}
+
+constexpr int kLoaders = kWaves - 1;   // wavefronts 1..3 stream tiles
+constexpr int kSlots = 2;              // chunk buffers in LDS
+enum SlotState : int { kSlotFree = 0, kSlotLoading = 1, kSlotReady = 2, kSlotEnd = 3 };
+// slot metadata words
+constexpr int kMetaSeq = 0, kMetaState = 1, kMetaGroup = 2, kMetaChunk = 3, kMetaDone = 4, kMetaAbort = 5;
+
+__device__ __forceinline__ int lds_ld(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_st(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Phase 2 for one chunk (resolver wavefront).  `tiles` holds the chunk's tile
+// records, `aggbuf` the loaders' partial aggregates (nagg of them).
+template <int G>
+__device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* tiles,
+                              const float* aggbuf, int nagg, int lane) {
+  constexpr int REC = Cfg<G>::REC;
+  const GroupInfo gi = group_info(P, gidx);
+  const int b = gi.b, kvh = gi.kvh, T = gi.T, n_chunks = gi.n_chunks;
   const int C = P.chunk_blocks;
-  const int n_chunks = (T + C - 1) / C;
-  if (n_chunks == 0) {
-    if (khint == 0) write_empty<G>(P, b, kvh);
-    return;
-  }
-  if (khint >= n_chunks) return;
-
-  if (tid == 0) {
-    const uint32_t k = __hip_atomic_fetch_add(P.claim + gidx, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if ((int)k == n_chunks - 1)  // last claim of this call: reset for the next call
-      __hip_atomic_store(P.claim + gidx, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    int ex = 0;
-    if (ld_relaxed(P.stop_epoch + gidx) == P.epoch) {
-      acquire_agent();
-      ex = (int)ld_relaxed32(P.stop_chunk + gidx) < (int)k;
-    }
-    s_claim = (int)k;
-    s_exit = ex;
-  }
-  __syncthreads();
-  const int k = s_claim;
-  if (s_exit) return;
-  if (k >= n_chunks) {  // the workspace was not zero-filled: refuse rather than index past it
-    if (tid == 0) __hip_atomic_store(P.error_word, 7u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
-
-  const int t0 = k * C;                 // first traversal step (0-based) of the chunk
+  const int t0 = k * C;
   const int nb = min(C, T - t0);
   const int tpb = P.tiles_per_block;
-  const int ntiles = nb * tpb;
-  float* tiles = smem;
-  float* pbuf = smem + P.chunk_tiles_lds * REC + wave * (kTile * G);
+  const __amdgpu_buffer_rsrc_t rs = record_rsrc(P, gidx);
+  const int rec_agg = k * 2 * P.record_floats;          // float offsets in the group's area
+  const int rec_inc = rec_agg + P.record_floats;
+  int32_t* stab_me = P.stab + ((int64_t)gidx * P.max_chunks + k) * 8;
 
-  {
-    bf16x8 qa[4];
-    load_q<G>(P, b, kvh, lane, qa);
-    for (int ti = wave; ti < ntiles; ti += kWaves) {
-      const int i = ti / tpb, j = ti - i * tpb;
-      const int step = t0 + i;
-      int blk;
-      if (list) {
-        blk = list[step];
-        blk = blk < 0 ? 0 : (blk >= nblk ? nblk - 1 : blk);
-      } else {
-        blk = P.dense_order == 1 ? step : nblk - 1 - step;
-      }
-      compute_tile<G>(P, b, kvh, L, blk * Bk + j * kTile, qa, pbuf, tiles + ti * REC);
-    }
-  }
-  __syncthreads();
-  if (wave != 0) return;
-
-  // ---------------- phase 2: wave 0 ----------------
-  float* rec_agg = P.records + ((int64_t)gidx * P.max_chunks + k) * 2 * P.record_floats;
-  float* rec_inc = rec_agg + P.record_floats;
-
-  // chunk aggregate: left fold over blocks, each block a left fold over tiles
+  // chunk aggregate: w0 (+) (w1 (+) w2) over the loaders' partials, or a
+  // left fold over the tiles when the partials did not fit in LDS
   State<G> agg;
-  state_clear<G>(agg);
-  for (int i = 0; i < nb; ++i) {
-    State<G> blkst, t;
-    state_clear<G>(blkst);
-    for (int j = 0; j < tpb; ++j) {
-      read_tile<G>(tiles + (i * tpb + j) * REC, t, lane);
-      merge<G, false>(blkst, t);
+  if (nagg == kLoaders) {
+    State<G> a1, a2;
+    read_state<G>(aggbuf + 0 * REC, agg, lane);
+    read_state<G>(aggbuf + 1 * REC, a1, lane);
+    read_state<G>(aggbuf + 2 * REC, a2, lane);
+    merge<G, false>(a1, a2);
+    merge<G, false>(agg, a1);
+  } else {
+    State<G> t;
+    state_clear<G>(agg);
+    for (int ti = 0; ti < nb * tpb; ++ti) {
+      read_tile<G>(tiles + ti * REC, t, lane);
+      merge<G, false>(agg, t);
     }
-    merge<G, false>(agg, blkst);
   }
-  write_state<G>(rec_agg, agg, lane);
-  publish(P, gidx, k, kAggregate, lane);
 
-  // softmax look-back: nearest chunk with an inclusive state, then fold forward
-  int j = k - 1;
-  while (j >= 0) {
-    const int st = wait_state(P, gidx, j, kAggregate, k);
-    if (st < 0) return;
-    if (st >= (int)kInclusive) break;
-    --j;
+  // Fast path: the previous chunk is fully resolved (or there is none), so
+  // the prefix and the entering stability state are known now and all four
+  // records go out with a single publication.  Otherwise publish the
+  // aggregate first so that later chunks can fold past this one.
+  const bool fast = (k == 0) ||
+      flag_state(ld_relaxed(P.flags + (int64_t)gidx * P.max_chunks + (k - 1)), P.epoch) >= kStabInclusive;
+  if (!fast) {
+    publish_state<G>(rs, rec_agg, agg, lane);
+    publish(P, gidx, k, kAggregate, lane);
   }
-  acquire_agent();
+
+  // softmax prefix: nearest chunk with an inclusive state, then the
+  // aggregates after it folded forward (four records in flight at a time)
+  int j = fast ? k - 1 : lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
+  if (j == -2) return;
+  compiler_fence();
   State<G> pre;
   if (j >= 0) {
-    read_state<G>(P.records + ((int64_t)gidx * P.max_chunks + j) * 2 * P.record_floats + P.record_floats, pre, lane);
+    fetch_state<G>(rs, j * 2 * P.record_floats + P.record_floats, pre, lane);
   } else {
     state_clear<G>(pre);
   }
-  for (int i = j + 1; i < k; ++i) {
-    State<G> a;
-    read_state<G>(P.records + ((int64_t)gidx * P.max_chunks + i) * 2 * P.record_floats, a, lane);
-    merge<G, false>(pre, a);
-  }
-  {
-    State<G> inc = pre;
-    merge<G, false>(inc, agg);
-    write_state<G>(rec_inc, inc, lane);
-    publish(P, gidx, k, kInclusive, lane);
+  for (int i0 = j + 1; i0 < k; i0 += 4) {
+    const int n = min(4, k - i0);
+    State<G> a[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (u < n) fetch_state<G>(rs, (i0 + u) * 2 * P.record_floats, a[u], lane);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (u < n) merge<G, false>(pre, a[u]);
   }
 
   // replay the chunk's blocks from the prefix with the stability test
@@ -654,15 +755,15 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         od = row_sum(od);
         n1 = row_sum(n1);
         // Eq. (2): d_scale = |d|; d_direction = 1 - cos(o_new, o_old)
-        const float d_scale = __fsqrt_rn(dd);
-        const float nn = __fmul_rn(__fsqrt_rn(n1), __fsqrt_rn(n0));
+        const float d_scale = fast_sqrt(dd);
+        const float nn = __fmul_rn(fast_sqrt(n1), fast_sqrt(n0));
         const float dot = __fadd_rn(n0, od);
         float d_dir;
         if (dot > 0.f) {
           const float num = fmaxf(__fsub_rn(__fmul_rn(n0, dd), __fmul_rn(od, od)), 0.f);
-          d_dir = __fdiv_rn(num, __fmul_rn(nn, __fadd_rn(nn, dot)));
+          d_dir = __fmul_rn(num, fast_rcp(__fmul_rn(nn, __fadd_rn(nn, dot))));
         } else {
-          d_dir = __fsub_rn(1.f, __fdiv_rn(dot, nn));
+          d_dir = __fsub_rn(1.f, __fmul_rn(dot, fast_rcp(nn)));
         }
         const bool st = (n0 > 0.f) && (n1 > 0.f) && (d_scale < P.tau) && (d_dir < P.phi);
         if (slot_valid<G>(lane, kk) && !st) ok = false;
@@ -692,60 +793,262 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
     sm.len = nb;
     sm.fis = fis;
   }
-  int32_t* stab_me = P.stab + ((int64_t)gidx * P.max_chunks + k) * 8;
+  {
+    State<G> inc = pre;
+    merge<G, false>(inc, agg);
+    if (fast) publish_state<G>(rs, rec_agg, agg, lane);
+    publish_state<G>(rs, rec_inc, inc, lane);
+  }
   if (lane == 0) {
-    stab_me[0] = sm.lead;
-    stab_me[1] = sm.trail;
-    stab_me[2] = sm.len;
-    stab_me[3] = sm.fis;
+    st_coh_i32(stab_me + 0, sm.lead);
+    st_coh_i32(stab_me + 1, sm.trail);
+    st_coh_i32(stab_me + 2, sm.len);
+    st_coh_i32(stab_me + 3, sm.fis);
   }
-  publish(P, gidx, k, kStabSummary, lane);
 
-  // stability look-back
-  j = k - 1;
-  while (j >= 0) {
-    const int st = wait_state(P, gidx, j, kStabSummary, k);
-    if (st < 0) return;
-    if (st >= (int)kStabInclusive) break;
-    --j;
+  // entering stability state: nearest chunk with an inclusive stability
+  // state, then the summaries after it (fetched one per lane)
+  if (!fast) {
+    publish(P, gidx, k, kStabSummary, lane);
+    j = lookback_scan(P, gidx, k, kStabSummary, kStabInclusive, lane);
+    if (j == -2) return;
+    compiler_fence();
   }
-  acquire_agent();
   StabState x{0, 0, 0, 0};
   if (j >= 0) {
     const int32_t* sj = P.stab + ((int64_t)gidx * P.max_chunks + j) * 8;
-    x.stopped = sj[4];
-    x.stop_t = sj[5];
-    x.run = sj[6];
+    x.stopped = ld_coh_i32(sj + 4);
+    x.stop_t = ld_coh_i32(sj + 5);
+    x.run = ld_coh_i32(sj + 6);
   }
-  for (int i = j + 1; i < k; ++i) {
-    const int32_t* si = P.stab + ((int64_t)gidx * P.max_chunks + i) * 8;
-    StabSummary y{si[0], si[1], si[2], si[3]};
-    x = stab_fold(x, y, i * C, P.patience);
+  for (int i0 = j + 1; i0 < k; i0 += 64) {
+    const int n = min(64, k - i0);
+    int32_t y0 = 0, y1 = 0, y2 = 0, y3 = 0;
+    if (lane < n) {
+      const int32_t* si = P.stab + ((int64_t)gidx * P.max_chunks + i0 + lane) * 8;
+      y0 = ld_coh_i32(si + 0);
+      y1 = ld_coh_i32(si + 1);
+      y2 = ld_coh_i32(si + 2);
+      y3 = ld_coh_i32(si + 3);
+    }
+    for (int u = 0; u < n; ++u) {
+      const StabSummary y{__builtin_amdgcn_readlane(y0, u), __builtin_amdgcn_readlane(y1, u),
+                          __builtin_amdgcn_readlane(y2, u), __builtin_amdgcn_readlane(y3, u)};
+      x = stab_fold(x, y, (i0 + u) * C, P.patience);
+    }
   }
   const bool stopped_before = x.stopped != 0;
   const StabState y = stab_fold(x, sm, t0, P.patience);
   if (lane == 0) {
-    stab_me[4] = y.stopped;
-    stab_me[5] = y.stop_t;
-    stab_me[6] = y.run;
+    st_coh_i32(stab_me + 4, y.stopped);
+    st_coh_i32(stab_me + 5, y.stop_t);
+    st_coh_i32(stab_me + 6, y.run);
   }
+  publish(P, gidx, k, kStabInclusive, lane);
+  if (lane == 0)
+    __hip_atomic_fetch_max(P.resolved + gidx, (P.epoch << 24) | (uint64_t)(k + 1),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  wave_lds_sync();  // saved per-block states were written by other lanes
   if (!stopped_before && y.stopped) {
-    // the stop lies in this chunk: write o(t*) and announce the stop
+    // the stop lies in this chunk: announce it, then write o(t*)
+    if (lane == 0)
+      __hip_atomic_store(P.stop_chunk + gidx, (uint32_t)k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    stores_complete();
+    if (lane == 0)
+      __hip_atomic_store(P.stop_epoch + gidx, P.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     State<G> s;
     read_state<G>(tiles + (y.stop_t - 1 - t0) * tpb * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, y.stop_t, lane);
-    if (lane == 0) {
-      __hip_atomic_store(P.stop_chunk + gidx, (uint32_t)k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    release_agent();
-    if (lane == 0)
-      __hip_atomic_store(P.stop_epoch + gidx, P.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   } else if (!y.stopped && k == n_chunks - 1) {
     State<G> s;
     read_state<G>(tiles + (nb - 1) * tpb * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, T, lane);
   }
-  publish(P, gidx, k, kStabInclusive, lane);
+}
+
+// ---- the kernel -----------------------------------------------------------------
+// Persistent workgroups of four wavefronts.  Wavefronts 1..3 claim chunks
+// (strided over the chunk-major work list) and stream their tiles into one
+// of two LDS chunk buffers; wavefront 0 resolves the previous chunk at the
+// same time.  A chunk is claimed only once a buffer is free, and every wait
+// targets a chunk claimed earlier, so the launch always makes progress.
+template <int G>
+__global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
+  extern __shared__ float smem[];
+  __shared__ int s_meta[kSlots][8];
+  constexpr int REC = Cfg<G>::REC;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int n_groups = P.batch * P.num_kv_heads;
+  const int CT = P.chunk_tiles_lds;
+  const int nagg = P.loader_partials;
+  const int slot_floats = (CT + nagg) * REC;
+  float* pbuf_all = smem + kSlots * slot_floats;
+
+  if (tid < kSlots * 8) (&s_meta[0][0])[tid] = (tid % 8 == kMetaSeq) ? -1 : 0;
+  __syncthreads();
+
+  if (wave == 0) {
+    // ---------------- resolver ----------------
+    __builtin_amdgcn_s_setprio(3);
+    for (int it = 0;; ++it) {
+      const int slot = it & 1;
+      int st = kSlotFree;
+      for (uint32_t spin = 0;; ++spin) {
+        st = lds_ld(&s_meta[slot][kMetaState]);
+        if (lds_ld(&s_meta[slot][kMetaSeq]) == it && (st == kSlotReady || st == kSlotEnd)) break;
+        if (spin >= P.spin_limit) {
+          __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          return;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (st == kSlotEnd) return;
+      const int gidx = lds_ld(&s_meta[slot][kMetaGroup]);
+      const int k = lds_ld(&s_meta[slot][kMetaChunk]);
+      if (!lds_ld(&s_meta[slot][kMetaAbort])) {
+        float* base = smem + slot * slot_floats;
+        resolve_chunk<G>(P, gidx, k, base, base + CT * REC, nagg, lane);
+      }
+      wave_lds_sync();
+      if (lane == 0) lds_st(&s_meta[slot][kMetaState], kSlotFree);
+    }
+  }
+
+  // ---------------- loaders ----------------
+  const int lw = wave - 1;
+  float* pbuf = pbuf_all + lw * (kTile * G);
+  const int q_total = n_groups * P.max_chunks;
+  int q = blockIdx.x;  // next index of the chunk-major work list (leader only)
+  for (int it = 0;; ++it) {
+    const int slot = it & 1;
+    if (lw == 0) {
+      // leader: wait for the buffer, then claim the next chunk of the list
+      bool gave_up = false;
+      for (uint32_t spin = 0; lds_ld(&s_meta[slot][kMetaState]) != kSlotFree; ++spin) {
+        if (spin >= P.spin_limit) {
+          __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          gave_up = true;  // hand out the end marker below
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      int gsel = -1, ksel = -1;
+      while (!gave_up && q < q_total) {
+        const int g = q % n_groups, kh = q / n_groups;
+        q += gridDim.x;
+        const GroupInfo gi = group_info(P, g);
+        if (gi.n_chunks == 0) {
+          if (kh == 0) write_empty_wave<G>(P, gi.b, gi.kvh, lane);
+          continue;
+        }
+        if (kh >= gi.n_chunks) continue;
+        uint32_t claimed = 0;
+        if (lane == 0) {
+          claimed = __hip_atomic_fetch_add(P.claim + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if ((int)claimed == gi.n_chunks - 1)  // last claim of the call: reset for the next call
+            __hip_atomic_store(P.claim + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const int kc = __builtin_amdgcn_readfirstlane((int)claimed);
+        if (kc >= gi.n_chunks) {  // the workspace was not zero-filled
+          if (lane == 0) __hip_atomic_store(P.error_word, 7u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          continue;
+        }
+        if (stop_announced_before(P, g, kc)) continue;
+        gsel = g;
+        ksel = kc;
+        break;
+      }
+      if (lane == 0) {
+        lds_st(&s_meta[slot][kMetaGroup], gsel);
+        lds_st(&s_meta[slot][kMetaChunk], ksel);
+        lds_st(&s_meta[slot][kMetaDone], 0);
+        lds_st(&s_meta[slot][kMetaAbort], 0);
+      }
+      wave_lds_sync();
+      if (lane == 0) {
+        lds_st(&s_meta[slot][kMetaState], gsel >= 0 ? kSlotLoading : kSlotEnd);
+        lds_st(&s_meta[slot][kMetaSeq], it);
+      }
+    }
+    // every loader: wait for this iteration's assignment
+    int st = kSlotFree;
+    for (uint32_t spin = 0;; ++spin) {
+      st = lds_ld(&s_meta[slot][kMetaState]);
+      if (lds_ld(&s_meta[slot][kMetaSeq]) == it && (st == kSlotLoading || st == kSlotEnd)) break;
+      if (spin >= P.spin_limit) {
+        __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (st == kSlotEnd) return;
+    const int gidx = lds_ld(&s_meta[slot][kMetaGroup]);
+    const int k = lds_ld(&s_meta[slot][kMetaChunk]);
+    const GroupInfo gi = group_info(P, gidx);
+    const int t0 = k * P.chunk_blocks;
+    const int nb = min(P.chunk_blocks, gi.T - t0);
+    const int tpb = P.tiles_per_block;
+    const int ntiles = nb * tpb;
+    float* tiles = smem + slot * slot_floats;
+    bool aborted = false;
+    {
+      bf16x8 qa[4];
+      load_q<G>(P, gi.b, gi.kvh, lane, qa);
+      // the block list entry and the pages of every tile this wave streams,
+      // fetched together once per chunk: lane 4m + n covers 16-token group n
+      // of the wave's m-th tile (at most 16 tiles per wave)
+      int my_tok0 = 0x7fffffff, my_page = 0;
+      {
+        const int m = lane >> 2, n = lane & 3;
+        const int ti = lw + kLoaders * m;
+        if (ti < ntiles) {
+          const int i = ti / tpb, j = ti - i * tpb;
+          const int step = t0 + i;
+          int blk;
+          if (gi.list) {
+            blk = gi.list[step];
+            blk = blk < 0 ? 0 : (blk >= gi.nblk ? gi.nblk - 1 : blk);
+          } else {
+            blk = P.dense_order == 1 ? step : gi.nblk - 1 - step;
+          }
+          my_tok0 = blk * P.block_size + j * kTile;
+          if (my_tok0 < gi.L) my_page = clamp_page(P, gi.b, min(my_tok0 + 16 * n, gi.L - 1));
+        }
+      }
+      for (int ti = lw, m = 0; ti < ntiles; ti += kLoaders, ++m) {
+        // a stop announced by an earlier chunk makes this chunk's work moot;
+        // the flag read here completes while the tile's loads are in flight
+        const uint64_t se = ld_relaxed(P.stop_epoch + gidx);
+        const int tok0 = __builtin_amdgcn_readlane(my_tok0, 4 * m);
+        const int pg[4] = {__builtin_amdgcn_readlane(my_page, 4 * m), __builtin_amdgcn_readlane(my_page, 4 * m + 1),
+                           __builtin_amdgcn_readlane(my_page, 4 * m + 2), __builtin_amdgcn_readlane(my_page, 4 * m + 3)};
+        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, pbuf, tiles + ti * REC);
+        if (se == P.epoch && (int)ld_relaxed32(P.stop_chunk + gidx) < k) {
+          aborted = true;
+          break;
+        }
+      }
+    }
+    wave_lds_sync();
+    if (aborted) {
+      if (lane == 0) lds_st(&s_meta[slot][kMetaAbort], 1);
+    } else if (nagg == kLoaders) {
+      // this loader's tiles folded in tile order: a partial aggregate
+      State<G> wagg, t;
+      state_clear<G>(wagg);
+      for (int ti = lw; ti < ntiles; ti += kLoaders) {
+        read_tile<G>(tiles + ti * REC, t, lane);
+        merge<G, false>(wagg, t);
+      }
+      write_state<G>(tiles + CT * REC + lw * REC, wagg, lane);
+    }
+    wave_lds_sync();
+    if (lane == 0) {
+      const int done = __hip_atomic_fetch_add(&s_meta[slot][kMetaDone], 1, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (done == kLoaders - 1) lds_st(&s_meta[slot][kMetaState], kSlotReady);
+    }
+  }
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n_words) {
@@ -755,8 +1058,16 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n_words) {
 
 template <int G>
 int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
-  const int64_t grid = (int64_t)plan.n_groups * plan.max_chunks;
-  if (grid <= 0) return (int)hipSuccess;
+  const int64_t work = (int64_t)plan.n_groups * plan.max_chunks;
+  if (work <= 0) return (int)hipSuccess;
+  int dev = 0, cus = 0, per_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, art_decode_kernel<G>, kThreads, plan.lds_bytes);
+  if (e != hipSuccess) return (int)e;
+  if (per_cu < 1) per_cu = 1;
+  const int64_t grid = min(work, (int64_t)cus * per_cu);
   hipLaunchKernelGGL(art_decode_kernel<G>, dim3((unsigned)grid), dim3(kThreads),
                      plan.lds_bytes, stream, params);
   return (int)hipGetLastError();
