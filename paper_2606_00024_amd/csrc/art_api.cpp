@@ -100,11 +100,13 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
         C = 8 / tpb;
         if (C < 1) C = 1;
         while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
+        // the work list must fit the queue word
+        while (C < c_max && n_groups * ((t_cap + C - 1) / C) + art::kQueueSlack >= (1 << art::kQueueBits)) C *= 2;
     }
     if (C > c_max) C = c_max;
     if (C < 1) C = 1;
     const int64_t max_chunks = (t_cap + C - 1) / C;
-    if (n_groups * max_chunks > INT32_MAX) return ART_ERR_UNSUPPORTED;
+    if (n_groups * max_chunks + art::kQueueSlack >= (1 << art::kQueueBits)) return ART_ERR_UNSUPPORTED;
 
     p->group = g;
     p->tiles_per_block = tpb;
@@ -119,10 +121,8 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     art::WorkspaceLayout& w = p->ws;
     size_t off = 0;
     w.error_off = off;      off = align_up(off + 4);
-    w.claim_off = off;      off = align_up(off + 4 * (size_t)n_groups);
-    w.stop_epoch_off = off; off = align_up(off + 8 * (size_t)n_groups);
-    w.stop_chunk_off = off; off = align_up(off + 4 * (size_t)n_groups);
-    w.resolved_off = off;   off = align_up(off + 8 * (size_t)n_groups);
+    w.queue_off = off;      off = align_up(off + 8);
+    w.stop_off = off;       off = align_up(off + 8 * (size_t)n_groups);
     w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
     w.stab_off = off;       off = align_up(off + 32 * (size_t)n_groups * max_chunks);
     w.records_off = off;    off = align_up(off + (size_t)n_groups * max_chunks * 2 * p->record_floats * 4);
@@ -211,6 +211,15 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.chunk_blocks = plan.chunk_blocks;
     k.max_chunks = plan.max_chunks;
     k.t_cap = plan.t_cap;
+    {
+        // the work list covers the longest traversal this call can have
+        const int64_t cap_tokens = (int64_t)shape->max_pages_per_seq * shape->page_size;
+        int64_t t_eff = block_list ? shape->max_blocks_per_list
+                                   : (cap_tokens + shape->block_size - 1) / shape->block_size;
+        if (t_eff > plan.t_cap) t_eff = plan.t_cap;
+        if (t_eff < 1) t_eff = 1;
+        k.work_chunks = (int32_t)((t_eff + plan.chunk_blocks - 1) / plan.chunk_blocks);
+    }
     k.record_floats = plan.record_floats;
     k.chunk_tiles_lds = plan.chunk_blocks * plan.tiles_per_block;
     k.loader_partials = plan.loader_partials;
@@ -226,10 +235,8 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.stop_block = stop_block;
     char* ws = static_cast<char*>(workspace);
     k.error_word = reinterpret_cast<uint32_t*>(ws + plan.ws.error_off);
-    k.claim = reinterpret_cast<uint32_t*>(ws + plan.ws.claim_off);
-    k.stop_epoch = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_epoch_off);
-    k.stop_chunk = reinterpret_cast<uint32_t*>(ws + plan.ws.stop_chunk_off);
-    k.resolved = reinterpret_cast<uint64_t*>(ws + plan.ws.resolved_off);
+    k.queue = reinterpret_cast<uint64_t*>(ws + plan.ws.queue_off);
+    k.stop_word = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_off);
     k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
     k.stab = reinterpret_cast<int32_t*>(ws + plan.ws.stab_off);
     k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
@@ -306,7 +313,7 @@ art_status art_workspace_status(const void* workspace, size_t workspace_bytes, h
     uint32_t word = 0;
     if (hipStreamSynchronize(stream) != hipSuccess) return ART_ERR_HIP;
     if (hipMemcpy(&word, workspace, 4, hipMemcpyDeviceToHost) != hipSuccess) return ART_ERR_HIP;
-    *device_status = word == 0 ? ART_OK : (word == 7 ? ART_ERR_INVALID_ARG : ART_ERR_DEVICE_TIMEOUT);
+    *device_status = word == 0 ? ART_OK : ART_ERR_DEVICE_TIMEOUT;
     return ART_OK;
 }
 

@@ -14,6 +14,10 @@ constexpr int kTile = 64;       // tokens one wavefront processes per tile
 constexpr int kWaves = 4;       // wavefronts per workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxChunkTiles = 16;
+// Work-list indices live in the low 24 bits of the queue word; a launch
+// hands out at most its list length plus one final index per workgroup.
+constexpr int kQueueBits = 24;
+constexpr int64_t kQueueSlack = 1 << 16;
 
 // Progress of one chunk, published in the low 3 bits of its flag word (the
 // rest of the word holds the call's epoch).  States only ever increase.
@@ -28,10 +32,8 @@ enum ChunkState : uint32_t {
 // Byte layout of a workspace (all offsets from its start, 256-aligned).
 struct WorkspaceLayout {
     size_t error_off;        // uint32 error word
-    size_t claim_off;        // uint32 [groups] chunk-claim counters
-    size_t stop_epoch_off;   // uint64 [groups] epoch of the announced stop
-    size_t stop_chunk_off;   // uint32 [groups] chunk that holds the stop
-    size_t resolved_off;     // uint64 [groups] epoch << 24 | resolved chunks
+    size_t queue_off;        // uint64 work-queue word: epoch << 24 | next index
+    size_t stop_off;         // uint64 [groups] announced stop: epoch << 24 | chunk
     size_t flags_off;        // uint64 [groups][max_chunks]
     size_t stab_off;         // int32 [groups][max_chunks][8]
     size_t records_off;      // float [groups][max_chunks][2][record_floats]
@@ -63,6 +65,7 @@ struct KernelParams {
     int32_t patience, dense_order, out_bf16;
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
+    int32_t work_chunks;     // chunk rows of the work list (<= max_chunks)
     int32_t chunk_tiles_lds; // tile records per LDS chunk buffer
     int32_t loader_partials; // per-loader partial aggregates kept in LDS (3 or 0)
     // data
@@ -78,10 +81,8 @@ struct KernelParams {
     int32_t* stop_block;
     // workspace
     uint32_t* error_word;
-    uint32_t* claim;
-    uint64_t* stop_epoch;
-    uint32_t* stop_chunk;
-    uint64_t* resolved;
+    uint64_t* queue;
+    uint64_t* stop_word;
     uint64_t* flags;
     int32_t* stab;
     float* records;

@@ -513,10 +513,12 @@ __device__ __forceinline__ StabState stab_fold(StabState x, StabSummary y, int t
   return r;
 }
 
+// The stop announcement of a group is one word: epoch << 24 | chunk.
+__device__ __forceinline__ bool stop_word_before(uint64_t v, uint64_t epoch, int me) {
+  return (v >> kQueueBits) == epoch && (int)(v & ((1ull << kQueueBits) - 1ull)) < me;
+}
 __device__ __forceinline__ bool stop_announced_before(const KernelParams& P, int gidx, int me) {
-  if (ld_relaxed(P.stop_epoch + gidx) != P.epoch) return false;
-  compiler_fence();
-  return (int)ld_relaxed32(P.stop_chunk + gidx) < me;
+  return stop_word_before(ld_relaxed(P.stop_word + gidx), P.epoch, me);
 }
 
 // Look-back over the flags of chunks me-1, me-2, ... of group gidx, 64 per
@@ -652,6 +654,52 @@ __device__ __forceinline__ void lds_st(int* p, int v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
+// Next index of the launch's chunk-major work list (index q is chunk
+// q / groups of group q % groups), taken from the workspace's queue word
+// (call epoch << 24 | next index) by one fetch-and-add (claim_issue; the
+// result is decoded by claim_finish).  A word left by an earlier call is replaced by
+// compare-and-swap with this call's epoch and index 1, which hands out
+// index 0; claims that raced with the replacement retry.  Indices are handed
+// out in increasing order and every workgroup takes them in that order, so a
+// chunk only ever waits on chunks that some workgroup holds.  Lane 0 only /
+// wave-uniform result.
+__device__ __forceinline__ uint64_t claim_issue(const KernelParams& P, int lane) {
+  return lane == 0 ? __hip_atomic_fetch_add(P.queue, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+}
+
+__device__ int claim_finish(const KernelParams& P, uint64_t v, int lane) {
+  int q = 0;
+  if (lane == 0) {
+    const uint64_t mask = (1ull << kQueueBits) - 1ull;
+    if ((v >> kQueueBits) == P.epoch) {
+      q = (int)(v & mask);
+    } else {
+      uint64_t cur = v + 1ull;
+      for (uint32_t spin = 0;; ++spin) {
+        if ((cur >> kQueueBits) == P.epoch) {
+          v = __hip_atomic_fetch_add(P.queue, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if ((v >> kQueueBits) == P.epoch) {
+            q = (int)(v & mask);
+            break;
+          }
+          cur = v + 1ull;
+        } else if (__hip_atomic_compare_exchange_strong(P.queue, &cur, (P.epoch << kQueueBits) | 1ull,
+                                                        __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT)) {
+          q = 0;
+          break;
+        }
+        if (spin >= P.spin_limit) {
+          __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          q = 0x7fffffff;
+          break;
+        }
+      }
+    }
+  }
+  return __builtin_amdgcn_readfirstlane(q);
+}
+
 // Phase 2 for one chunk (resolver wavefront).  `tiles` holds the chunk's tile
 // records, `aggbuf` the loaders' partial aggregates (nagg of them).
 template <int G>
@@ -688,21 +736,24 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
     }
   }
 
-  // Fast path: the previous chunk is fully resolved (or there is none), so
-  // the prefix and the entering stability state are known now and all four
-  // records go out with a single publication.  Otherwise publish the
-  // aggregate first so that later chunks can fold past this one.
-  const bool fast = (k == 0) ||
-      flag_state(ld_relaxed(P.flags + (int64_t)gidx * P.max_chunks + (k - 1)), P.epoch) >= kStabInclusive;
-  if (!fast) {
+  // Softmax prefix.  Chunk 0 has an empty prefix; when chunk k-1 already
+  // holds its inclusive state the prefix is that record; otherwise publish
+  // the aggregate first (so that later chunks can fold past this one), look
+  // back to the nearest inclusive state and fold the aggregates after it
+  // forward, four records in flight at a time.  Every path computes the
+  // same left fold Agg(0) (+) ... (+) Agg(k-1), so the bits never depend on
+  // timing.
+  int j;
+  if (k == 0) {
+    j = -1;
+  } else if (flag_state(ld_relaxed(P.flags + (int64_t)gidx * P.max_chunks + (k - 1)), P.epoch) >= kInclusive) {
+    j = k - 1;
+  } else {
     publish_state<G>(rs, rec_agg, agg, lane);
     publish(P, gidx, k, kAggregate, lane);
+    j = lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
+    if (j == -2) return;
   }
-
-  // softmax prefix: nearest chunk with an inclusive state, then the
-  // aggregates after it folded forward (four records in flight at a time)
-  int j = fast ? k - 1 : lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
-  if (j == -2) return;
   compiler_fence();
   State<G> pre;
   if (j >= 0) {
@@ -720,15 +771,32 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
     for (int u = 0; u < 4; ++u)
       if (u < n) merge<G, false>(pre, a[u]);
   }
+  // the inclusive state goes out before the replay: it is all that later
+  // chunks need for their own prefix
+  {
+    State<G> inc = pre;
+    merge<G, false>(inc, agg);
+    publish_state<G>(rs, rec_inc, inc, lane);
+    publish(P, gidx, k, kInclusive, lane);
+  }
 
   // replay the chunk's blocks from the prefix with the stability test
   uint32_t stable_bits = 0;
   {
     State<G> s = pre;
+    // |o|^2 per head slot of the state before the next block
+    float n_prev[Cfg<G>::HPL];
+#pragma unroll
+    for (int kk = 0; kk < Cfg<G>::HPL; ++kk) {
+      float n0 = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n0);
+      n_prev[kk] = row_sum(n0);
+    }
     for (int i = 0; i < nb; ++i) {
       State<G> blkst, t;
-      state_clear<G>(blkst);
-      for (int jj = 0; jj < tpb; ++jj) {
+      read_tile<G>(tiles + (i * tpb) * REC, blkst, lane);
+      for (int jj = 1; jj < tpb; ++jj) {
         read_tile<G>(tiles + (i * tpb + jj) * REC, t, lane);
         merge<G, false>(blkst, t);
       }
@@ -742,18 +810,18 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
       bool ok = true;
 #pragma unroll
       for (int kk = 0; kk < Cfg<G>::HPL; ++kk) {
-        float n0 = 0.f, dd = 0.f, od = 0.f, n1 = 0.f;
+        float dd = 0.f, od = 0.f, n1 = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          n0 = __builtin_fmaf(old_o[kk][e], old_o[kk][e], n0);
           dd = __builtin_fmaf(d[kk][e], d[kk][e], dd);
           od = __builtin_fmaf(old_o[kk][e], d[kk][e], od);
           n1 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n1);
         }
-        n0 = row_sum(n0);
+        const float n0 = n_prev[kk];
         dd = row_sum(dd);
         od = row_sum(od);
         n1 = row_sum(n1);
+        n_prev[kk] = n1;
         // Eq. (2): d_scale = |d|; d_direction = 1 - cos(o_new, o_old)
         const float d_scale = fast_sqrt(dd);
         const float nn = __fmul_rn(fast_sqrt(n1), fast_sqrt(n0));
@@ -793,27 +861,23 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
     sm.len = nb;
     sm.fis = fis;
   }
-  {
-    State<G> inc = pre;
-    merge<G, false>(inc, agg);
-    if (fast) publish_state<G>(rs, rec_agg, agg, lane);
-    publish_state<G>(rs, rec_inc, inc, lane);
-  }
   if (lane == 0) {
     st_coh_i32(stab_me + 0, sm.lead);
     st_coh_i32(stab_me + 1, sm.trail);
     st_coh_i32(stab_me + 2, sm.len);
     st_coh_i32(stab_me + 3, sm.fis);
   }
+  publish(P, gidx, k, kStabSummary, lane);
+  // A chunk whose first block is unstable and whose own run never reaches
+  // the patience cannot hold the stop, whatever run it enters with: unless
+  // it is the last chunk (which writes the untruncated result) it is done.
+  if (sm.lead == 0 && sm.fis < 0 && k != n_chunks - 1) return;
 
   // entering stability state: nearest chunk with an inclusive stability
   // state, then the summaries after it (fetched one per lane)
-  if (!fast) {
-    publish(P, gidx, k, kStabSummary, lane);
-    j = lookback_scan(P, gidx, k, kStabSummary, kStabInclusive, lane);
-    if (j == -2) return;
-    compiler_fence();
-  }
+  j = lookback_scan(P, gidx, k, kStabSummary, kStabInclusive, lane);
+  if (j == -2) return;
+  compiler_fence();
   StabState x{0, 0, 0, 0};
   if (j >= 0) {
     const int32_t* sj = P.stab + ((int64_t)gidx * P.max_chunks + j) * 8;
@@ -845,17 +909,12 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
     st_coh_i32(stab_me + 6, y.run);
   }
   publish(P, gidx, k, kStabInclusive, lane);
-  if (lane == 0)
-    __hip_atomic_fetch_max(P.resolved + gidx, (P.epoch << 24) | (uint64_t)(k + 1),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   wave_lds_sync();  // saved per-block states were written by other lanes
   if (!stopped_before && y.stopped) {
     // the stop lies in this chunk: announce it, then write o(t*)
     if (lane == 0)
-      __hip_atomic_store(P.stop_chunk + gidx, (uint32_t)k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    stores_complete();
-    if (lane == 0)
-      __hip_atomic_store(P.stop_epoch + gidx, P.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(P.stop_word + gidx, (P.epoch << kQueueBits) | (uint64_t)k, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     State<G> s;
     read_state<G>(tiles + (y.stop_t - 1 - t0) * tpb * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, y.stop_t, lane);
@@ -917,8 +976,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   // ---------------- loaders ----------------
   const int lw = wave - 1;
   float* pbuf = pbuf_all + lw * (kTile * G);
-  const int q_total = n_groups * P.max_chunks;
-  int q = blockIdx.x;  // next index of the chunk-major work list (leader only)
+  const int q_total = n_groups * P.work_chunks;
   for (int it = 0;; ++it) {
     const int slot = it & 1;
     if (lw == 0) {
@@ -933,29 +991,18 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         __builtin_amdgcn_s_sleep(1);
       }
       int gsel = -1, ksel = -1;
-      while (!gave_up && q < q_total) {
+      while (!gave_up) {
+        const int q = claim_finish(P, claim_issue(P, lane), lane);
+        if (q >= q_total) break;
         const int g = q % n_groups, kh = q / n_groups;
-        q += gridDim.x;
         const GroupInfo gi = group_info(P, g);
         if (gi.n_chunks == 0) {
           if (kh == 0) write_empty_wave<G>(P, gi.b, gi.kvh, lane);
           continue;
         }
-        if (kh >= gi.n_chunks) continue;
-        uint32_t claimed = 0;
-        if (lane == 0) {
-          claimed = __hip_atomic_fetch_add(P.claim + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if ((int)claimed == gi.n_chunks - 1)  // last claim of the call: reset for the next call
-            __hip_atomic_store(P.claim + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        const int kc = __builtin_amdgcn_readfirstlane((int)claimed);
-        if (kc >= gi.n_chunks) {  // the workspace was not zero-filled
-          if (lane == 0) __hip_atomic_store(P.error_word, 7u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          continue;
-        }
-        if (stop_announced_before(P, g, kc)) continue;
+        if (kh >= gi.n_chunks || stop_announced_before(P, g, kh)) continue;
         gsel = g;
-        ksel = kc;
+        ksel = kh;
         break;
       }
       if (lane == 0) {
@@ -1018,12 +1065,12 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       for (int ti = lw, m = 0; ti < ntiles; ti += kLoaders, ++m) {
         // a stop announced by an earlier chunk makes this chunk's work moot;
         // the flag read here completes while the tile's loads are in flight
-        const uint64_t se = ld_relaxed(P.stop_epoch + gidx);
+        const uint64_t sw = ld_relaxed(P.stop_word + gidx);
         const int tok0 = __builtin_amdgcn_readlane(my_tok0, 4 * m);
         const int pg[4] = {__builtin_amdgcn_readlane(my_page, 4 * m), __builtin_amdgcn_readlane(my_page, 4 * m + 1),
                            __builtin_amdgcn_readlane(my_page, 4 * m + 2), __builtin_amdgcn_readlane(my_page, 4 * m + 3)};
         compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, pbuf, tiles + ti * REC);
-        if (se == P.epoch && (int)ld_relaxed32(P.stop_chunk + gidx) < k) {
+        if (stop_word_before(sw, P.epoch, k)) {
           aborted = true;
           break;
         }
