@@ -33,6 +33,29 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, published
 
+# HBM bytes per launch of the decode kernel counted by rocprofv3 (FETCH_SIZE
+# scaled by 2.0 plus WRITE_SIZE scaled by 1.0: the factors a plain 1 GiB
+# device copy gives for those counters), per workload and mode at the
+# workload's default thresholds.  They hold only for the sources they were
+# counted on, identified by SHA-256; after any change to those sources the
+# figure is reported as null until it is counted again.
+COUNTED_TRAFFIC = {
+    "sources_sha256": "8bda589186e013b8c109cd590e9d9e4570b301ce37d0bf80073b0885f9b4c048",
+    "bytes": {("llama3_8b_32k", "on"): 592408928, ("llama3_8b_32k", "off"): 1132412800},
+}
+TRAFFIC_SOURCES = ("art_kernels.hip", "art_api.cpp", "art_internal.h")
+
+
+def counted_traffic(workload, mode):
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_00024_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != COUNTED_TRAFFIC["sources_sha256"]:
+        return None
+    return COUNTED_TRAFFIC["bytes"].get((workload, mode))
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -223,10 +246,13 @@ def main():
     off = None if args.no_off else measure(0.0, phi, pat, max(5, args.steps // 2), max(2, args.warmup // 2))
     cpu = None if args.no_cpu else cpu_baseline(wl, eligible_tokens, tau, phi, pat, args.cpu_seconds)
 
-    def roofline(r):
+    defaults = (tau, phi, pat) == (spec.tau, spec.phi, spec.patience) and args.chunk_blocks == 0
+
+    def roofline(r, mode):
         ach = r["hbm_gbps_on_bytes_read"]
+        traffic = counted_traffic(args.workload, mode) if defaults else None
         return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBPS, "traffic": None,
+                "frac": ach / HBM_PEAK_GBPS, "traffic": traffic,
                 "kernel": "art_decode_kernel<4>", "kernel_ms": r["kernel_ms"],
                 "alg_bytes_per_launch": r["alg_bytes_per_launch"]}
 
@@ -250,9 +276,9 @@ def main():
         "skipped_pct": on["skipped_pct"],
         "read_tokens_heads_per_s": on["read_tokens_heads_per_s"],
         "kernel_ms": on["kernel_ms"],
-        "roofline": roofline(on),
+        "roofline": roofline(on, "on"),
         "cpu_baseline": cpu,
-        "termination_off": None if off is None else dict(off, roofline=roofline(off)),
+        "termination_off": None if off is None else dict(off, roofline=roofline(off, "off")),
     }
     print(json.dumps(line), flush=True)
 
