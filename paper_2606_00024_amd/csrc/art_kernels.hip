@@ -8,42 +8,42 @@
 //
 // Work decomposition
 //   A group's traversal of T blocks is cut into chunks of C consecutive
-//   blocks.  One workgroup (4 wavefronts) handles one chunk; the grid is
-//   chunk-major (blockIdx = chunk_hint * groups + group) so that the early
-//   chunks of every group are dispatched first.  The order in which a
-//   group's chunks start is fixed by a per-group claim counter, so a chunk
-//   only ever waits on chunks that are already running: no deadlock whatever
-//   the dispatch order.
+//   blocks.  The chunks of all groups form one chunk-major work list (chunk
+//   0 of every group, then chunk 1, ...).  The grid is persistent (as many
+//   workgroups as the chip holds); workgroups take list indices from one
+//   epoch-tagged queue word, so workgroups freed by groups that stopped early
+//   move on to the groups that stop late.  Indices are handed out in order,
+//   so a chunk only ever waits on chunks some workgroup already holds: no
+//   deadlock whatever the dispatch order.
 //
-//   A chunk starts loading only within a window of chunks past the group's
-//   resolved frontier, which bounds the reads wasted past a stop.
+//   Loaders (wavefronts 1..3): the leader claims a chunk when one of two LDS
+//   chunk buffers is free; the loaders stream its 64-token tiles from HBM
+//   (16-byte loads, four 64-byte row segments per K load instruction, four
+//   256-byte rows per V load instruction), compute the scores of all g query
+//   heads with v_mfma_f32_16x16x32_bf16 (query heads are the M rows, tokens
+//   the N columns, head dims the reduction), the tile softmax in base 2 with
+//   row reductions over DPP, and P.V on the VALU in fp32, and leave (m, l,
+//   sum p v) for each tile in LDS.  Chunks after an announced stop are not
+//   loaded.
 //
-//   Phase 1 (all 4 wavefronts): each streams 64-token tiles of the chunk's
-//   blocks from HBM (16-byte loads, four 64-byte row segments per K load
-//   instruction, four 256-byte rows per V load instruction), computes the
-//   scores of all g query heads with v_mfma_f32_16x16x32_bf16 (query heads
-//   are the M rows, tokens the N columns, head dims the reduction), the tile
-//   softmax in base 2 with row reductions over DPP, and P.V on the VALU in
-//   fp32, and leaves (m, l, sum p v) for its tile in LDS.
-//
-//   Phase 2 (wavefront 0; the other three retire):
-//     - folds the tiles into block partials and the chunk aggregate and
-//       publishes the aggregate;
-//     - obtains the softmax state after the previous chunk by looking back
-//       to the nearest chunk that published its inclusive state and folding
-//       the aggregates in between forward.  Because the fold is always
-//       left-to-right over the same aggregates, every chunk computes the
-//       same bits for a given prefix: results do not depend on timing;
+//   Resolver (wavefront 0), per ready chunk:
+//     - folds the loaders' partials into the chunk aggregate;
+//     - obtains the softmax state after the previous chunk (that chunk's
+//       inclusive state, or the nearest inclusive state found by looking
+//       back with the aggregates after it folded forward: always the same
+//       left fold, so results never depend on timing) and publishes its own
+//       inclusive state at once;
 //     - replays its blocks from that prefix, running the stability test per
 //       block (normalised running output o(t), increment d = o(t) - o(t-1),
 //       d_scale = |d|, d_direction = 1 - cos from |o|^2, |d|^2 and o.d
 //       without cancellation);
-//     - publishes a stability summary, looks back the same way over the
-//       stability states (entering patience run, stop already found), and
-//       either stops inside the chunk (writes out/lse/stop_block and
-//       announces the stop so that later chunks skip their loads), or, as
-//       the last chunk, writes the untruncated result.
-//   Cross-workgroup data goes through the workspace with agent-coherent
+//     - publishes a stability summary; if the chunk can hold the stop (or is
+//       the group's last chunk) it looks back the same way over the
+//       stability states (entering patience run, stop already found) and
+//       either stops inside the chunk (announces the stop so that later
+//       chunks skip their loads, then writes out/lse/stop_block) or, as the
+//       last chunk, writes the untruncated result.
+//   Cross-workgroup data goes through the workspace with device-coherent
 //   accesses only, as the XCDs of MI355X have separate L2 caches (see the
 //   workspace helpers below).
 #include <hip/hip_runtime.h>
