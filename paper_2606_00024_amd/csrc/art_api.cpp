@@ -7,6 +7,8 @@
 #include <string.h>
 
 #include <atomic>
+#include <chrono>
+#include <random>
 #include <vector>
 
 #include "art_internal.h"
@@ -21,7 +23,20 @@ constexpr uint32_t kSpinLimit = 1u << 22;  // polls (~seconds) before a wait giv
 
 // Process-wide call counter: every launch tags the flags it writes with a
 // fresh value, so flags left by earlier calls are never mistaken for current.
-std::atomic<uint64_t> g_epoch{0};
+// It starts at a random point of [2^38, 2^39): the words of a workspace that
+// earlier held another layout (small integers, float bits) cannot pass for a
+// current tag, and 2^39 calls remain before the 2^40 limit of the tags.
+uint64_t initial_epoch() {
+    std::random_device rd;
+    uint64_t r = ((uint64_t)rd() << 32) ^ rd();
+    r ^= (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+    return (uint64_t(1) << 38) | (r & ((uint64_t(1) << 38) - 1));
+}
+
+uint64_t next_epoch() {
+    static std::atomic<uint64_t> counter{initial_epoch()};
+    return counter.fetch_add(1, std::memory_order_relaxed);
+}
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -240,7 +255,7 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
     k.stab = reinterpret_cast<int32_t*>(ws + plan.ws.stab_off);
     k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
-    k.epoch = g_epoch.fetch_add(1, std::memory_order_relaxed) + 1;
+    k.epoch = next_epoch();
     k.spin_limit = kSpinLimit;
     if (k.epoch >= (uint64_t(1) << 40)) return ART_ERR_UNSUPPORTED;
     return art::launch_decode(plan, k, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;

@@ -560,7 +560,6 @@ __device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, 
     __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, (P.epoch << 3) | state,
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
 template <int G>
 __device__ void write_outputs(const KernelParams& P, int b, int kvh, const State<G>& s,
                               int stop, int lane) {
@@ -740,9 +739,11 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
   // holds its inclusive state the prefix is that record; otherwise publish
   // the aggregate first (so that later chunks can fold past this one), look
   // back to the nearest inclusive state and fold the aggregates after it
-  // forward, four records in flight at a time.  Every path computes the
-  // same left fold Agg(0) (+) ... (+) Agg(k-1), so the bits never depend on
+  // forward, FW records in flight at a time.  Every path computes the same
+  // left fold Agg(0) (+) ... (+) Agg(k-1), so the bits never depend on
   // timing.
+  constexpr int HPL = Cfg<G>::HPL;
+  constexpr int FW = 8 / HPL > 0 ? 8 / HPL : 1;
   int j;
   if (k == 0) {
     j = -1;
@@ -761,84 +762,117 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
   } else {
     state_clear<G>(pre);
   }
-  for (int i0 = j + 1; i0 < k; i0 += 4) {
-    const int n = min(4, k - i0);
-    State<G> a[4];
+  for (int i0 = j + 1; i0 < k; i0 += FW) {
+    const int n = min(FW, k - i0);
+    State<G> a[FW];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < FW; ++u)
       if (u < n) fetch_state<G>(rs, (i0 + u) * 2 * P.record_floats, a[u], lane);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < FW; ++u)
       if (u < n) merge<G, false>(pre, a[u]);
   }
-  // the inclusive state goes out before the replay: it is all that later
-  // chunks need for their own prefix
+  // this chunk's inclusive state; its flag goes out during the replay
   {
     State<G> inc = pre;
     merge<G, false>(inc, agg);
     publish_state<G>(rs, rec_inc, inc, lane);
-    publish(P, gidx, k, kInclusive, lane);
   }
+  bool incl_pending = true;
+  auto raise_inclusive = [&]() {
+    publish(P, gidx, k, kInclusive, lane);
+    incl_pending = false;
+  };
 
-  // replay the chunk's blocks from the prefix with the stability test
+  // Replay the chunk's blocks from the prefix with the stability test.
+  // Blocks go in batches of NB: the merges run in order (each needs the
+  // state after the previous block) and leave per-lane partial sums; the
+  // row reductions of the whole batch then run together.
+  constexpr int NB = 8 / HPL > 0 ? 8 / HPL : 1;
   uint32_t stable_bits = 0;
   {
     State<G> s = pre;
     // |o|^2 per head slot of the state before the next block
-    float n_prev[Cfg<G>::HPL];
+    float n_prev[HPL];
 #pragma unroll
-    for (int kk = 0; kk < Cfg<G>::HPL; ++kk) {
+    for (int kk = 0; kk < HPL; ++kk) {
       float n0 = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n0);
       n_prev[kk] = row_sum(n0);
     }
-    for (int i = 0; i < nb; ++i) {
-      State<G> blkst, t;
-      read_tile<G>(tiles + (i * tpb) * REC, blkst, lane);
-      for (int jj = 1; jj < tpb; ++jj) {
-        read_tile<G>(tiles + (i * tpb + jj) * REC, t, lane);
-        merge<G, false>(blkst, t);
-      }
-      float old_o[Cfg<G>::HPL][8];
+    for (int i0 = 0; i0 < nb; i0 += NB) {
+      float pdd[NB][HPL], pod[NB][HPL], pn1[NB][HPL];
 #pragma unroll
-      for (int kk = 0; kk < Cfg<G>::HPL; ++kk)
+      for (int u = 0; u < NB; ++u) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) old_o[kk][e] = s.o[kk][e];
-      float d[Cfg<G>::HPL][8];
-      merge<G, true>(s, blkst, d);
-      bool ok = true;
+        for (int kk = 0; kk < HPL; ++kk) pdd[u][kk] = pod[u][kk] = pn1[u][kk] = 0.f;
+        const int i = i0 + u;
+        if (i < nb) {
+          State<G> blkst, t;
+          read_tile<G>(tiles + (i * tpb) * REC, blkst, lane);
+          for (int jj = 1; jj < tpb; ++jj) {
+            read_tile<G>(tiles + (i * tpb + jj) * REC, t, lane);
+            merge<G, false>(blkst, t);
+          }
+          float old_o[HPL][8];
 #pragma unroll
-      for (int kk = 0; kk < Cfg<G>::HPL; ++kk) {
-        float dd = 0.f, od = 0.f, n1 = 0.f;
+          for (int kk = 0; kk < HPL; ++kk)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          dd = __builtin_fmaf(d[kk][e], d[kk][e], dd);
-          od = __builtin_fmaf(old_o[kk][e], d[kk][e], od);
-          n1 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n1);
+            for (int e = 0; e < 8; ++e) old_o[kk][e] = s.o[kk][e];
+          float d[HPL][8];
+          merge<G, true>(s, blkst, d);
+#pragma unroll
+          for (int kk = 0; kk < HPL; ++kk) {
+            float dd = 0.f, od = 0.f, n1 = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              dd = __builtin_fmaf(d[kk][e], d[kk][e], dd);
+              od = __builtin_fmaf(old_o[kk][e], d[kk][e], od);
+              n1 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n1);
+            }
+            pdd[u][kk] = dd;
+            pod[u][kk] = od;
+            pn1[u][kk] = n1;
+          }
+          write_state<G>(tiles + i * tpb * REC, s, lane);   // o(t) after block i, for the output
         }
-        const float n0 = n_prev[kk];
-        dd = row_sum(dd);
-        od = row_sum(od);
-        n1 = row_sum(n1);
-        n_prev[kk] = n1;
-        // Eq. (2): d_scale = |d|; d_direction = 1 - cos(o_new, o_old)
-        const float d_scale = fast_sqrt(dd);
-        const float nn = __fmul_rn(fast_sqrt(n1), fast_sqrt(n0));
-        const float dot = __fadd_rn(n0, od);
-        float d_dir;
-        if (dot > 0.f) {
-          const float num = fmaxf(__fsub_rn(__fmul_rn(n0, dd), __fmul_rn(od, od)), 0.f);
-          d_dir = __fmul_rn(num, fast_rcp(__fmul_rn(nn, __fadd_rn(nn, dot))));
-        } else {
-          d_dir = __fsub_rn(1.f, __fmul_rn(dot, fast_rcp(nn)));
-        }
-        const bool st = (n0 > 0.f) && (n1 > 0.f) && (d_scale < P.tau) && (d_dir < P.phi);
-        if (slot_valid<G>(lane, kk) && !st) ok = false;
       }
-      const bool all_ok = __all(ok);
-      stable_bits |= (all_ok ? 1u : 0u) << i;
-      write_state<G>(tiles + i * tpb * REC, s, lane);   // o(t) after block i, for the output
+      if (incl_pending) raise_inclusive();
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+#pragma unroll
+        for (int kk = 0; kk < HPL; ++kk) {
+          pdd[u][kk] = row_sum(pdd[u][kk]);
+          pod[u][kk] = row_sum(pod[u][kk]);
+          pn1[u][kk] = row_sum(pn1[u][kk]);
+        }
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int i = i0 + u;
+        if (i >= nb) break;
+        bool ok = true;
+#pragma unroll
+        for (int kk = 0; kk < HPL; ++kk) {
+          const float n0 = n_prev[kk], dd = pdd[u][kk], od = pod[u][kk], n1 = pn1[u][kk];
+          n_prev[kk] = n1;
+          // Eq. (2): d_scale = |d|; d_direction = 1 - cos(o_new, o_old)
+          const float d_scale = fast_sqrt(dd);
+          const float nn = __fmul_rn(fast_sqrt(n1), fast_sqrt(n0));
+          const float dot = __fadd_rn(n0, od);
+          float d_dir;
+          if (dot > 0.f) {
+            const float num = fmaxf(__fsub_rn(__fmul_rn(n0, dd), __fmul_rn(od, od)), 0.f);
+            d_dir = __fmul_rn(num, fast_rcp(__fmul_rn(nn, __fadd_rn(nn, dot))));
+          } else {
+            d_dir = __fsub_rn(1.f, __fmul_rn(dot, fast_rcp(nn)));
+          }
+          const bool st = (n0 > 0.f) && (n1 > 0.f) && (d_scale < P.tau) && (d_dir < P.phi);
+          if (slot_valid<G>(lane, kk) && !st) ok = false;
+        }
+        const bool all_ok = __all(ok);
+        stable_bits |= (all_ok ? 1u : 0u) << i;
+      }
     }
   }
 

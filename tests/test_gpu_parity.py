@@ -223,6 +223,20 @@ def test_workspace_reuse_across_shapes():
     assert api.workspace_status(ws) == _lib.OK
 
 
+def test_workspace_reuse_through_every_layout():
+    """One workspace (zero-filled once) serves every small shape in turn under
+    two threshold settings: whatever an earlier call of another layout left in
+    the words a call uses as flags must not be taken for its own."""
+    ws = api.new_workspace(64 << 20, DEV)
+    for thr in (THRESHOLDS[0], THRESHOLDS[1]):
+        for case in SMALL:
+            wl = _small(case)
+            gpu = _run(wl, *thr, workspace=ws)
+            rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2])
+            assert rep.ok(), f"case s{case[0]} thr {thr}: {rep}"
+    assert api.workspace_status(ws) == _lib.OK
+
+
 # ------------------------------------------------------------ full-size workloads
 
 def _sample_groups(wl, n, seed):
