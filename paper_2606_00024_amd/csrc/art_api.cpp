@@ -90,14 +90,15 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     if (t_cap > INT32_MAX / 2) return ART_ERR_UNSUPPORTED;
     const int64_t n_groups = (int64_t)s->batch * s->num_kv_heads;
 
-    // LDS of a workgroup: two chunk buffers of C*tpb tile records plus three
-    // per-loader partial aggregates each (when they fit), and three P.V
-    // staging buffers.  Kept within 64 KiB.
+    // LDS of a workgroup: two or three chunk buffers of C*tpb tile records
+    // plus three per-loader partial aggregates each (when they fit), and
+    // three P.V staging buffers.  Kept within 78 KiB, so that two workgroups
+    // share a CU's 160 KiB.
     const size_t rec_bytes = (size_t)(g * art::kHeadDim + 2 * g) * 4;
     const size_t pbuf_bytes = (size_t)3 * art::kTile * g * 4;
-    const size_t lds_cap = 64 * 1024;
-    auto lds_for = [&](int tiles, int partials) {
-        return 2 * (size_t)(tiles + partials) * rec_bytes + pbuf_bytes;
+    const size_t lds_cap = 78 * 1024;
+    auto lds_for = [&](int tiles, int partials, int slots = 2) {
+        return slots * (size_t)(tiles + partials) * rec_bytes + pbuf_bytes;
     };
     int partials = 3;
     if (lds_for(tpb, partials) > lds_cap) partials = 0;
@@ -131,7 +132,10 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     p->t_cap = (int32_t)t_cap;
     p->record_floats = (g * art::kHeadDim + 2 * g + 63) / 64 * 64;
     p->loader_partials = partials;
-    p->lds_bytes = lds_for(C * tpb, partials);
+    // (a third buffer was measured: it lets loaders run further past a
+    // stop and gains nothing elsewhere)
+    p->slots = 2;
+    p->lds_bytes = lds_for(C * tpb, partials, p->slots);
 
     art::WorkspaceLayout& w = p->ws;
     size_t off = 0;
@@ -226,6 +230,7 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.chunk_blocks = plan.chunk_blocks;
     k.max_chunks = plan.max_chunks;
     k.t_cap = plan.t_cap;
+    k.n_slots = plan.slots;
     {
         // the work list covers the longest traversal this call can have
         const int64_t cap_tokens = (int64_t)shape->max_pages_per_seq * shape->page_size;

@@ -16,8 +16,8 @@
 //   so a chunk only ever waits on chunks some workgroup already holds: no
 //   deadlock whatever the dispatch order.
 //
-//   Loaders (wavefronts 1..3): the leader claims a chunk when one of two LDS
-//   chunk buffers is free; the loaders stream its 64-token tiles from HBM
+//   Loaders (wavefronts 1..3): the leader claims a chunk when one of the LDS
+//   chunk buffers (two or three) is free; the loaders stream its 64-token tiles from HBM
 //   (16-byte loads, four 64-byte row segments per K load instruction, four
 //   256-byte rows per V load instruction), compute the scores of all g query
 //   heads with v_mfma_f32_16x16x32_bf16 (query heads are the M rows, tokens
@@ -641,7 +641,7 @@ __device__ void write_empty_wave(const KernelParams& P, int b, int kvh, int lane
 }
 
 constexpr int kLoaders = kWaves - 1;   // wavefronts 1..3 stream tiles
-constexpr int kSlots = 2;              // chunk buffers in LDS
+constexpr int kMaxSlots = 3;           // chunk buffers in LDS (the plan picks 2 or 3)
 enum SlotState : int { kSlotFree = 0, kSlotLoading = 1, kSlotReady = 2, kSlotEnd = 3 };
 // slot metadata words
 constexpr int kMetaSeq = 0, kMetaState = 1, kMetaGroup = 2, kMetaChunk = 3, kMetaDone = 4, kMetaAbort = 5;
@@ -961,30 +961,31 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
 
 // ---- the kernel -----------------------------------------------------------------
 // Persistent workgroups of four wavefronts.  Wavefronts 1..3 claim chunks
-// (strided over the chunk-major work list) and stream their tiles into one
-// of two LDS chunk buffers; wavefront 0 resolves the previous chunk at the
-// same time.  A chunk is claimed only once a buffer is free, and every wait
-// targets a chunk claimed earlier, so the launch always makes progress.
+// from the work list and stream their tiles into the LDS chunk buffers in
+// turn; wavefront 0 resolves earlier chunks meanwhile.  A chunk is claimed
+// only once a buffer is free, and every wait targets a chunk claimed
+// earlier, so the launch always makes progress.
 template <int G>
 __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
   extern __shared__ float smem[];
-  __shared__ int s_meta[kSlots][8];
+  __shared__ int s_meta[kMaxSlots][8];
   constexpr int REC = Cfg<G>::REC;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int n_groups = P.batch * P.num_kv_heads;
   const int CT = P.chunk_tiles_lds;
   const int nagg = P.loader_partials;
   const int slot_floats = (CT + nagg) * REC;
-  float* pbuf_all = smem + kSlots * slot_floats;
+  const int n_slots = P.n_slots;
+  float* pbuf_all = smem + n_slots * slot_floats;
 
-  if (tid < kSlots * 8) (&s_meta[0][0])[tid] = (tid % 8 == kMetaSeq) ? -1 : 0;
+  if (tid < kMaxSlots * 8) (&s_meta[0][0])[tid] = (tid % 8 == kMetaSeq) ? -1 : 0;
   __syncthreads();
 
   if (wave == 0) {
     // ---------------- resolver ----------------
     __builtin_amdgcn_s_setprio(3);
     for (int it = 0;; ++it) {
-      const int slot = it & 1;
+      const int slot = it % n_slots;
       int st = kSlotFree;
       for (uint32_t spin = 0;; ++spin) {
         st = lds_ld(&s_meta[slot][kMetaState]);
@@ -1012,7 +1013,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   float* pbuf = pbuf_all + lw * (kTile * G);
   const int q_total = n_groups * P.work_chunks;
   for (int it = 0;; ++it) {
-    const int slot = it & 1;
+    const int slot = it % n_slots;
     if (lw == 0) {
       // leader: wait for the buffer, then claim the next chunk of the list
       bool gave_up = false;
