@@ -92,19 +92,25 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
 
     // LDS of a workgroup: two or three chunk buffers of C*tpb tile records
     // plus three per-loader partial aggregates each (when they fit), and
-    // three P.V staging buffers.  Kept within 78 KiB, so that two workgroups
-    // share a CU's 160 KiB.
+    // three V staging buffers (32 rows of 288 bytes).  Kept within 78 KiB,
+    // so that two workgroups share a CU's 160 KiB.
     const size_t rec_bytes = (size_t)(g * art::kHeadDim + 2 * g) * 4;
-    const size_t pbuf_bytes = (size_t)3 * art::kTile * g * 4;
+    const size_t pbuf_bytes = (size_t)3 * 32 * 288 + 16;
     const size_t lds_cap = 78 * 1024;
     auto lds_for = [&](int tiles, int partials, int slots = 2) {
         return slots * (size_t)(tiles + partials) * rec_bytes + pbuf_bytes;
     };
-    int partials = 3;
-    if (lds_for(tpb, partials) > lds_cap) partials = 0;
-    if (lds_for(tpb, partials) > lds_cap) return ART_ERR_UNSUPPORTED;
-    int max_tiles = art::kMaxChunkTiles;
-    while (max_tiles > tpb && lds_for(max_tiles, partials) > lds_cap) --max_tiles;
+    // the per-loader partials save the resolver a fold over the tiles; they
+    // are kept unless dropping them lets a chunk hold more tiles (up to 8)
+    auto tiles_fitting = [&](int partials) {
+        int t = art::kMaxChunkTiles;
+        while (t > 0 && lds_for(t, partials) > lds_cap) --t;
+        return t;
+    };
+    const int t3 = tiles_fitting(3), t0 = tiles_fitting(0);
+    const int partials = (t3 >= tpb && t3 >= (t0 < 8 ? t0 : 8)) ? 3 : 0;
+    const int max_tiles = partials ? t3 : t0;
+    if (max_tiles < tpb) return ART_ERR_UNSUPPORTED;
     const int c_max = max_tiles / tpb;
 
     int C;

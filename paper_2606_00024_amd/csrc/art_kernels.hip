@@ -339,14 +339,29 @@ __device__ __forceinline__ int clamp_page(const KernelParams& P, int b, int tok)
   return pg >= P.num_pages ? P.num_pages - 1 : pg;
 }
 
-// Writes into `rec` (LDS): sum_j p_hj v_j [G][128], m_h [G] (base 2), l_h [G].
-// pg[n] is the (uniform) physical page of the 16-token group n of the tile.
+// A 64-token tile on one wavefront.  Both contractions run on
+// v_mfma_f32_16x16x32_bf16:
+//   - scores transposed, S^T = K Q^T (tokens are the M rows, the query
+//     heads of the group the N columns, head dims the reduction), so that
+//     each lane ends up holding the probabilities of one head for exactly
+//     the eight tokens that the P.V A-operand needs from it;
+//   - P.V with P as A (heads x 32 tokens) and V as B (32 tokens x 16 dims).
+//     V reaches the B layout (eight tokens of one dim per lane) through LDS:
+//     each half tile is written row-major and read back with
+//     ds_read_b64_tr_b16.  P is split into three bf16 parts (hi + mid + lo
+//     carries 24 significant bits), so P.V keeps fp32 precision.
+// The record written to LDS holds sum_j p_hj v_j [G][128], m_h [G] (base 2),
+// l_h [G].  pg[n] is the (uniform) physical page of 16-token group n.
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+constexpr int kVPitch = 144;                  // u16 per row of the V staging buffer (288 B)
+constexpr int kVBufU16 = 32 * kVPitch;        // one half tile: 32 rows
+
 template <int G>
 __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, const int (&pg)[4],
-                             const bf16x8 (&qa)[4], float* __restrict__ pbuf,
+                             const bf16x8 (&qa)[4], uint16_t* __restrict__ vbuf,
                              float* __restrict__ rec) {
   const int lane = threadIdx.x & 63;
-  const int lo = lane & 15, hi = lane >> 4;
+  const int lo = lane & 15, g = lane >> 4;
   const int psz_mask = (1 << P.page_shift) - 1;
 
   if (tok0 >= L) {  // tile past the sequence end: empty partial
@@ -358,10 +373,11 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
     return;
   }
 
-  // K: for 16-token group n, lane holds token 16n + lo, dims chunk 4s + hi.
+  // K: for 16-token group n, lane holds token 16n + lo, dims 32s + 8g .. +7.
   // A 16-aligned group never straddles a page (page_size >= 16, power of
   // two); tokens past L are redirected to token L-1, which lies in the same
-  // group or in the last group before it, so one page serves the group.
+  // group or in the last group before it, the group whose page pg[n] then
+  // names.
   u32x4 kr[4][4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) {
@@ -370,116 +386,125 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
                          (int64_t)(tok & psz_mask) * P.ks_tok;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      kr[n][s] = *reinterpret_cast<const u32x4*>(kp + (4 * s + hi) * 8);
+      kr[n][s] = *reinterpret_cast<const u32x4*>(kp + (4 * s + g) * 8);
   }
-  // V: lane (lo, hi) holds tokens 16*hi + i, dims 8*lo .. +7.  Issued with
-  // the K loads so that one memory latency covers the whole tile.
+  // V: lane (lo, g) holds token 4i + g, dims 8lo .. +7; the four tokens of
+  // one load instruction are consecutive and lie in group i / 4.  Issued
+  // with the K loads so that one memory latency covers the whole tile.
   u32x4 vr[16];
   {
-    const int pgv = hi == 0 ? pg[0] : (hi == 1 ? pg[1] : (hi == 2 ? pg[2] : pg[3]));
-    const uint16_t* vp = P.v + (int64_t)pgv * P.vs_page + (int64_t)kvh * P.vs_head + lo * 8;
+    const uint16_t* vp = P.v + (int64_t)kvh * P.vs_head + lo * 8;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int tok = min(tok0 + 16 * hi + i, L - 1);
-      vr[i] = *reinterpret_cast<const u32x4*>(vp + (int64_t)(tok & psz_mask) * P.vs_tok);
+      const int tok = min(tok0 + 4 * i + g, L - 1);
+      vr[i] = *reinterpret_cast<const u32x4*>(vp + (int64_t)pg[i >> 2] * P.vs_page +
+                                              (int64_t)(tok & psz_mask) * P.vs_tok);
     }
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // Scores: S[n] = Q (16 head rows) x K^T (16 token columns), K = 128 dims.
-  f32x4 S[4];
+  // S^T[n][r]: token 16n + 4g + r, head lo.
+  f32x4 St[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) {
-    S[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    St[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      S[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[s], __builtin_bit_cast(bf16x8, kr[n][s]), S[n], 0, 0, 0);
+      St[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[n][s]), qa[s], St[n], 0, 0, 0);
   }
-  // S[n][r]: head 4*hi + r, token 16n + lo.
-  const int hb = 4 * hi;
-  float sc[4][4], mx[4], lsum[4];
+  // softmax of head lo over the tile: the lane's 16 tokens, then the four
+  // lanes lo, lo+16, lo+32, lo+48 (every lane of a column ends with the
+  // same bits: max is exact and each step adds the same two values)
+  float sc[4][4];
+  float mx = kNegInf;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float m = kNegInf;
+  for (int n = 0; n < 4; ++n)
 #pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      const bool ok = (hb + r < G) && (tok0 + 16 * n + lo < L);
-      sc[n][r] = ok ? S[n][r] * P.scale_log2 : kNegInf;
-      m = fmaxf(m, sc[n][r]);
+    for (int r = 0; r < 4; ++r) {
+      const bool ok = (lo < G) && (tok0 + 16 * n + 4 * g + r < L);
+      sc[n][r] = ok ? St[n][r] * P.scale_log2 : kNegInf;
+      mx = fmaxf(mx, sc[n][r]);
     }
-    mx[r] = row_max(m);
-  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  float ls = 0.f;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float acc = 0.f;
+  for (int n = 0; n < 4; ++n)
 #pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      const float p = mx[r] == kNegInf ? 0.f : fast_exp2(sc[n][r] - mx[r]);
+    for (int r = 0; r < 4; ++r) {
+      const float p = mx == kNegInf ? 0.f : fast_exp2(sc[n][r] - mx);
       sc[n][r] = p;
-      acc += p;
+      ls += p;
     }
-    lsum[r] = row_sum(acc);
+  ls = ls + __shfl_xor(ls, 16);
+  ls = ls + __shfl_xor(ls, 32);
+  if (g == 0 && lo < G) {
+    rec[G * kD + lo] = mx;
+    rec[G * kD + G + lo] = ls;
   }
-  // p to LDS as [token][head] for the P.V layout.
-  if (hb < G) {
-#pragma unroll
-    for (int n = 0; n < 4; ++n)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (hb + r < G) pbuf[(16 * n + lo) * G + hb + r] = sc[n][r];
-  }
-  if (lo == 0 && hb < G) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (hb + r < G) {
-        rec[G * kD + hb + r] = mx[r];
-        rec[G * kD + G + hb + r] = lsum[r];
-      }
-  }
-  wave_lds_sync();
 
-  // P.V: acc[h][e] over this lane's 16 tokens, then across the 4 rows.
-  constexpr int HC = Cfg<G>::HC;
+  // A operands of the two 32-token K-steps c: element e of lane (lo, g) is
+  // p of head lo at token 16(2c + e/4) + 4g + e%4, in three bf16 parts.
+  bf16x8 a[2][3];
 #pragma unroll
-  for (int hc0 = 0; hc0 < G; hc0 += HC) {
-    float acc[HC][8];
+  for (int c = 0; c < 2; ++c) {
+    uint32_t w[3][4];
 #pragma unroll
-    for (int h = 0; h < HC; ++h)
+    for (int e2 = 0; e2 < 4; ++e2) {
+      uint32_t part[3][2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+      for (int h = 0; h < 2; ++h) {
+        const int e = 2 * e2 + h;
+        const float p = sc[2 * c + (e >> 2)][e & 3];
+        const uint32_t b0 = f32_to_bf16_bits(p);
+        const float r1 = p - __uint_as_float(b0 << 16);
+        const uint32_t b1 = f32_to_bf16_bits(r1);
+        const float r2 = r1 - __uint_as_float(b1 << 16);
+        part[0][h] = b0;
+        part[1][h] = b1;
+        part[2][h] = f32_to_bf16_bits(r2);
+      }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float* pp = pbuf + (16 * hi + i) * G + hc0;
-      float pv[HC];
-#pragma unroll
-      for (int h = 0; h < HC; ++h) pv[h] = pp[h];
-      const u32x4 w = vr[i];
-      float v[8];
-      v[0] = bf_lo(w[0]); v[1] = bf_hi(w[0]); v[2] = bf_lo(w[1]); v[3] = bf_hi(w[1]);
-      v[4] = bf_lo(w[2]); v[5] = bf_hi(w[2]); v[6] = bf_lo(w[3]); v[7] = bf_hi(w[3]);
-#pragma unroll
-      for (int h = 0; h < HC; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = __builtin_fmaf(pv[h], v[e], acc[h][e]);
+      for (int j = 0; j < 3; ++j) w[j][e2] = part[j][0] | (part[j][1] << 16);
     }
 #pragma unroll
-    for (int h = 0; h < HC; ++h)
+    for (int j = 0; j < 3; ++j) a[c][j] = __builtin_bit_cast(bf16x8, u32x4{w[j][0], w[j][1], w[j][2], w[j][3]});
+  }
+
+  // P.V over the two halves of the tile.  B for K-step c and dims
+  // 16d .. 16d+15: lane (lo, g) needs V[token of element e][16d + lo]; in
+  // each 16-lane group, source lane 4k + q of a transposing read points at
+  // row 4g + k (then 16 + 4g + k), columns 16d + 4q .. +3.  The row pitch of
+  // 288 bytes puts the 16 lanes of a group on 32 distinct banks.
+  f32x4 acc[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float x = acc[h][e];
-        x = x + __shfl_xor(x, 16);
-        x = x + __shfl_xor(x, 32);
-        acc[h][e] = x;
-      }
+  for (int d = 0; d < 8; ++d) acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int rk = lo >> 2, cq = lo & 3;
 #pragma unroll
-    for (int h = 0; h < HC; ++h) {
-      const int hg = hc0 + h;
-      const int owner = G >= 4 ? (hg & 3) : hg;
-      if (owner == hi) {
-        f32x4* dst = reinterpret_cast<f32x4*>(rec + hg * kD + lo * 8);
-        dst[0] = f32x4{acc[h][0], acc[h][1], acc[h][2], acc[h][3]};
-        dst[1] = f32x4{acc[h][4], acc[h][5], acc[h][6], acc[h][7]};
-      }
+  for (int c = 0; c < 2; ++c) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      *reinterpret_cast<u32x4*>(vbuf + (4 * i + g) * kVPitch + 8 * lo) = vr[8 * c + i];
+    wave_lds_sync();
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const v4i16 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4i16*)(vbuf + (4 * g + rk) * kVPitch + 16 * d + 4 * cq));
+      const v4i16 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4i16*)(vbuf + (16 + 4 * g + rk) * kVPitch + 16 * d + 4 * cq));
+      const bf16x8 b = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+      for (int j = 0; j < 3; ++j) acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[c][j], b, acc[d], 0, 0, 0);
+    }
+    wave_lds_sync();  // the reads of this half complete before the next half is written
+  }
+  // acc[d][r]: head 4g + r, dim 16d + lo
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * g + r;
+    if (h < G) {
+#pragma unroll
+      for (int d = 0; d < 8; ++d) rec[h * kD + 16 * d + lo] = acc[d][r];
     }
   }
 }
@@ -976,7 +1001,8 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   const int nagg = P.loader_partials;
   const int slot_floats = (CT + nagg) * REC;
   const int n_slots = P.n_slots;
-  float* pbuf_all = smem + n_slots * slot_floats;
+  // V staging buffers of the loaders after the chunk buffers (16-byte aligned)
+  uint16_t* vbuf_all = reinterpret_cast<uint16_t*>(smem + ((n_slots * slot_floats + 3) & ~3));
 
   if (tid < kMaxSlots * 8) (&s_meta[0][0])[tid] = (tid % 8 == kMetaSeq) ? -1 : 0;
   __syncthreads();
@@ -1010,7 +1036,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
 
   // ---------------- loaders ----------------
   const int lw = wave - 1;
-  float* pbuf = pbuf_all + lw * (kTile * G);
+  uint16_t* vbuf = vbuf_all + lw * kVBufU16;
   const int q_total = n_groups * P.work_chunks;
   for (int it = 0;; ++it) {
     const int slot = it % n_slots;
@@ -1104,7 +1130,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         const int tok0 = __builtin_amdgcn_readlane(my_tok0, 4 * m);
         const int pg[4] = {__builtin_amdgcn_readlane(my_page, 4 * m), __builtin_amdgcn_readlane(my_page, 4 * m + 1),
                            __builtin_amdgcn_readlane(my_page, 4 * m + 2), __builtin_amdgcn_readlane(my_page, 4 * m + 3)};
-        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, pbuf, tiles + ti * REC);
+        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, vbuf, tiles + ti * REC);
         if (stop_word_before(sw, P.epoch, k)) {
           aborted = true;
           break;
