@@ -122,7 +122,7 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
         C = 8 / tpb;
         if (C < 1) C = 1;
         while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
-        // the work list must fit the queue word
+        // the work list must fit a queue word
         while (C < c_max && n_groups * ((t_cap + C - 1) / C) + art::kQueueSlack >= (1 << art::kQueueBits)) C *= 2;
     }
     if (C > c_max) C = c_max;
@@ -146,7 +146,7 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     art::WorkspaceLayout& w = p->ws;
     size_t off = 0;
     w.error_off = off;      off = align_up(off + 4);
-    w.queue_off = off;      off = align_up(off + 8);
+    w.queue_off = off;      off = align_up(off + 8 * art::kQueueStride * art::kQueues);
     w.stop_off = off;       off = align_up(off + 8 * (size_t)n_groups);
     w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
     w.stab_off = off;       off = align_up(off + 32 * (size_t)n_groups * max_chunks);

@@ -18,6 +18,10 @@ constexpr int kMaxChunkTiles = 16;
 // hands out at most its list length plus one final index per workgroup.
 constexpr int kQueueBits = 24;
 constexpr int64_t kQueueSlack = 1 << 16;
+// The work list is split over this many queue words (groups g with
+// g % kQueues == x go to queue x), each in its own 256-byte line.
+constexpr int kQueues = 8;
+constexpr int kQueueStride = 32;  // uint64 words between queue words
 
 // Progress of one chunk, published in the low 3 bits of its flag word (the
 // rest of the word holds the call's epoch).  States only ever increase.
@@ -32,7 +36,7 @@ enum ChunkState : uint32_t {
 // Byte layout of a workspace (all offsets from its start, 256-aligned).
 struct WorkspaceLayout {
     size_t error_off;        // uint32 error word
-    size_t queue_off;        // uint64 work-queue word: epoch << 24 | next index
+    size_t queue_off;        // kQueues work-queue words (one per 256 bytes): epoch << 24 | next index
     size_t stop_off;         // uint64 [groups] announced stop: epoch << 24 | chunk
     size_t flags_off;        // uint64 [groups][max_chunks]
     size_t stab_off;         // int32 [groups][max_chunks][8]

@@ -678,22 +678,31 @@ __device__ __forceinline__ void lds_st(int* p, int v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// Next index of the launch's chunk-major work list (index q is chunk
-// q / groups of group q % groups), taken from the workspace's queue word
-// (call epoch << 24 | next index) by one fetch-and-add (claim_issue; the
-// result is decoded by claim_finish).  A word left by an earlier call is replaced by
-// compare-and-swap with this call's epoch and index 1, which hands out
-// index 0; claims that raced with the replacement retry.  Indices are handed
-// out in increasing order and every workgroup takes them in that order, so a
-// chunk only ever waits on chunks that some workgroup holds.  Lane 0 only /
+// Work queues.  The chunks of the launch form kQueues chunk-major lists:
+// queue x holds the groups g with g % kQueues == x (n_x of them), and its
+// index i stands for chunk i / n_x of group x + kQueues * (i % n_x).  Each
+// list is handed out from its own workspace word (call epoch << 24 | next
+// index) by one fetch-and-add (claim_issue; claim_finish decodes it), so
+// that claims spread over kQueues atomic units.  A word left by an earlier
+// call is replaced by compare-and-swap with this call's epoch and index 1,
+// which hands out index 0; claims that raced with the replacement retry.
+// Every chunk a chunk can wait on belongs to the same group, hence to the
+// same list, and each list is handed out in increasing order: a chunk only
+// ever waits on chunks that some workgroup already holds.  Lane 0 only /
 // wave-uniform result.
-__device__ __forceinline__ uint64_t claim_issue(const KernelParams& P, int lane) {
-  return lane == 0 ? __hip_atomic_fetch_add(P.queue, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+__device__ __forceinline__ uint64_t* queue_word(const KernelParams& P, int x) {
+  return P.queue + (int64_t)x * kQueueStride;
 }
 
-__device__ int claim_finish(const KernelParams& P, uint64_t v, int lane) {
+__device__ __forceinline__ uint64_t claim_issue(const KernelParams& P, int x, int lane) {
+  return lane == 0 ? __hip_atomic_fetch_add(queue_word(P, x), 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                   : 0ull;
+}
+
+__device__ int claim_finish(const KernelParams& P, int x, uint64_t v, int lane) {
   int q = 0;
   if (lane == 0) {
+    uint64_t* w = queue_word(P, x);
     const uint64_t mask = (1ull << kQueueBits) - 1ull;
     if ((v >> kQueueBits) == P.epoch) {
       q = (int)(v & mask);
@@ -701,13 +710,13 @@ __device__ int claim_finish(const KernelParams& P, uint64_t v, int lane) {
       uint64_t cur = v + 1ull;
       for (uint32_t spin = 0;; ++spin) {
         if ((cur >> kQueueBits) == P.epoch) {
-          v = __hip_atomic_fetch_add(P.queue, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          v = __hip_atomic_fetch_add(w, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           if ((v >> kQueueBits) == P.epoch) {
             q = (int)(v & mask);
             break;
           }
           cur = v + 1ull;
-        } else if (__hip_atomic_compare_exchange_strong(P.queue, &cur, (P.epoch << kQueueBits) | 1ull,
+        } else if (__hip_atomic_compare_exchange_strong(w, &cur, (P.epoch << kQueueBits) | 1ull,
                                                         __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                                         __HIP_MEMORY_SCOPE_AGENT)) {
           q = 0;
@@ -1037,7 +1046,10 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   // ---------------- loaders ----------------
   const int lw = wave - 1;
   uint16_t* vbuf = vbuf_all + lw * kVBufU16;
-  const int q_total = n_groups * P.work_chunks;
+  // leader: the queue it claims from (its own first, then the others in
+  // turn once its own is used up) and the queues found used up
+  int qx = blockIdx.x % kQueues;
+  uint32_t used_up = 0;
   for (int it = 0;; ++it) {
     const int slot = it % n_slots;
     if (lw == 0) {
@@ -1052,10 +1064,15 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         __builtin_amdgcn_s_sleep(1);
       }
       int gsel = -1, ksel = -1;
-      while (!gave_up) {
-        const int q = claim_finish(P, claim_issue(P, lane), lane);
-        if (q >= q_total) break;
-        const int g = q % n_groups, kh = q / n_groups;
+      while (!gave_up && used_up != (1u << kQueues) - 1u) {
+        const int nx = (n_groups - qx + kQueues - 1) / kQueues;  // groups in queue qx
+        const int i = claim_finish(P, qx, claim_issue(P, qx, lane), lane);
+        if (i >= nx * P.work_chunks) {
+          used_up |= 1u << qx;
+          qx = (qx + 1) % kQueues;
+          continue;
+        }
+        const int g = qx + kQueues * (i % nx), kh = i / nx;
         const GroupInfo gi = group_info(P, g);
         if (gi.n_chunks == 0) {
           if (kh == 0) write_empty_wave<G>(P, gi.b, gi.kvh, lane);
