@@ -1049,7 +1049,8 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   // leader: the queue it claims from (its own first, then the others in
   // turn once its own is used up) and the queues found used up
   int qx = blockIdx.x % kQueues;
-  uint32_t used_up = 0;
+  uint64_t used_up = 0;
+  constexpr uint64_t kAllUsedUp = kQueues >= 64 ? ~0ull : ((1ull << kQueues) - 1ull);
   for (int it = 0;; ++it) {
     const int slot = it % n_slots;
     if (lw == 0) {
@@ -1064,11 +1065,11 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         __builtin_amdgcn_s_sleep(1);
       }
       int gsel = -1, ksel = -1;
-      while (!gave_up && used_up != (1u << kQueues) - 1u) {
+      while (!gave_up && used_up != kAllUsedUp) {
         const int nx = (n_groups - qx + kQueues - 1) / kQueues;  // groups in queue qx
         const int i = claim_finish(P, qx, claim_issue(P, qx, lane), lane);
         if (i >= nx * P.work_chunks) {
-          used_up |= 1u << qx;
+          used_up |= 1ull << qx;
           qx = (qx + 1) % kQueues;
           continue;
         }
