@@ -97,7 +97,9 @@ typedef struct {
  * patience = 1 is "no patience"; INT32_MAX runs the detector without ever
  * stopping.  chunk_blocks = 0 lets the library pick the split of each
  * traversal into chunks from the shape alone (never from the data or the
- * thresholds); 1..16 forces it.  The chunking changes rounding only.
+ * thresholds); 1..16 asks for that many blocks per chunk (capped at what
+ * the shared-memory budget holds for the shape).  The chunking changes
+ * rounding only.
  */
 typedef struct {
     float softmax_scale;           /* usually 1/sqrt(head_dim) (Eq. 1) */

@@ -61,7 +61,7 @@ art_status check_shape(const art_decode_shape* s, const art_decode_opts* o) {
     if (isnan(o->tau) || isnan(o->phi) || !isfinite(o->softmax_scale) || o->patience < 1 ||
         (o->dense_order != ART_ORDER_RECENT_FIRST && o->dense_order != ART_ORDER_FORWARD) ||
         (o->out_dtype != ART_OUT_F32 && o->out_dtype != ART_OUT_BF16) || o->chunk_blocks < 0 ||
-        o->chunk_blocks > art::kMaxChunkTiles)
+        o->chunk_blocks > art::kMaxChunkBlocks)
         return ART_ERR_INVALID_ARG;
     const int g = s->num_q_heads / s->num_kv_heads;
     if (s->head_dim != art::kHeadDim) return ART_ERR_UNSUPPORTED;
@@ -97,30 +97,30 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     const size_t rec_bytes = (size_t)(g * art::kHeadDim + 2 * g) * 4;
     const size_t pbuf_bytes = (size_t)3 * 32 * 288 + 16;
     const size_t lds_cap = 78 * 1024;
-    auto lds_for = [&](int tiles, int partials, int slots = 2) {
-        return slots * (size_t)(tiles + partials) * rec_bytes + pbuf_bytes;
+    auto lds_for = [&](int blocks, int partials, int slots = 2) {
+        return slots * (size_t)(blocks + partials) * rec_bytes + pbuf_bytes;
     };
-    // the per-loader partials save the resolver a fold over the tiles; they
-    // are kept unless dropping them lets a chunk hold more tiles (up to 8)
-    auto tiles_fitting = [&](int partials) {
-        int t = art::kMaxChunkTiles;
-        while (t > 0 && lds_for(t, partials) > lds_cap) --t;
-        return t;
+    // the per-loader partials save the resolver a fold over the blocks; they
+    // are kept unless dropping them lets a chunk hold more blocks (up to 8)
+    auto blocks_fitting = [&](int partials) {
+        int b = art::kMaxChunkBlocks;
+        while (b > 0 && lds_for(b, partials) > lds_cap) --b;
+        return b;
     };
-    const int t3 = tiles_fitting(3), t0 = tiles_fitting(0);
-    const int partials = (t3 >= tpb && t3 >= (t0 < 8 ? t0 : 8)) ? 3 : 0;
-    const int max_tiles = partials ? t3 : t0;
-    if (max_tiles < tpb) return ART_ERR_UNSUPPORTED;
-    const int c_max = max_tiles / tpb;
+    const int b3 = blocks_fitting(3), b0 = blocks_fitting(0);
+    const int partials = (b3 >= 1 && b3 >= (b0 < 8 ? b0 : 8)) ? 3 : 0;
+    int c_max = partials ? b3 : b0;
+    // a loader streams at most kMaxChunkTiles tiles of a chunk
+    while (c_max > 1 && (c_max + 2) / 3 * tpb > art::kMaxChunkTiles) --c_max;
+    if (c_max < 1) return ART_ERR_UNSUPPORTED;
 
     int C;
     if (o->chunk_blocks > 0) {
         C = o->chunk_blocks;
     } else {
-        // about 8 tiles per chunk; smaller chunks when the whole problem
+        // about 8 blocks per chunk; smaller chunks when the whole problem
         // would not give the 256 CUs enough work
-        C = 8 / tpb;
-        if (C < 1) C = 1;
+        C = 8;
         while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
         // the work list must fit a queue word
         while (C < c_max && n_groups * ((t_cap + C - 1) / C) + art::kQueueSlack >= (1 << art::kQueueBits)) C *= 2;
@@ -247,7 +247,7 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
         k.work_chunks = (int32_t)((t_eff + plan.chunk_blocks - 1) / plan.chunk_blocks);
     }
     k.record_floats = plan.record_floats;
-    k.chunk_tiles_lds = plan.chunk_blocks * plan.tiles_per_block;
+    k.chunk_recs_lds = plan.chunk_blocks;
     k.loader_partials = plan.loader_partials;
     k.q = static_cast<const uint16_t*>(q);
     k.k = static_cast<const uint16_t*>(k_cache);

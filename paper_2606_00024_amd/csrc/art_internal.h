@@ -13,7 +13,8 @@ constexpr int kHeadDim = 128;   // dims per head (the only supported value)
 constexpr int kTile = 64;       // tokens one wavefront processes per tile
 constexpr int kWaves = 4;       // wavefronts per workgroup
 constexpr int kThreads = 64 * kWaves;
-constexpr int kMaxChunkTiles = 16;
+constexpr int kMaxChunkTiles = 16;   // tiles one loader streams per chunk (and per block)
+constexpr int kMaxChunkBlocks = 16;  // blocks per chunk
 // Work-list indices live in the low 24 bits of the queue word; a launch
 // hands out at most its list length plus one final index per workgroup.
 constexpr int kQueueBits = 24;
@@ -71,7 +72,7 @@ struct KernelParams {
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
     int32_t work_chunks;     // chunk rows of the work list (<= max_chunks)
-    int32_t chunk_tiles_lds; // tile records per LDS chunk buffer
+    int32_t chunk_recs_lds;  // block records per LDS chunk buffer
     int32_t loader_partials; // per-loader partial aggregates kept in LDS (3 or 0)
     int32_t n_slots;         // chunk buffers in LDS (2 or 3)
     // data

@@ -356,15 +356,19 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 constexpr int kVPitch = 144;                  // u16 per row of the V staging buffer (288 B)
 constexpr int kVBufU16 = 32 * kVPitch;        // one half tile: 32 rows
 
+// The first tile of a block writes the block record; each later tile of
+// the block (accumulate) is folded into it: both parts rescaled to the
+// larger running max, in tile order.
 template <int G>
 __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, const int (&pg)[4],
                              const bf16x8 (&qa)[4], uint16_t* __restrict__ vbuf,
-                             float* __restrict__ rec) {
+                             float* __restrict__ rec, bool accumulate) {
   const int lane = threadIdx.x & 63;
   const int lo = lane & 15, g = lane >> 4;
   const int psz_mask = (1 << P.page_shift) - 1;
 
   if (tok0 >= L) {  // tile past the sequence end: empty partial
+    if (accumulate) return;
     for (int i = lane; i < G * kD; i += 64) rec[i] = 0.f;
     if (lane < G) {
       rec[G * kD + lane] = kNegInf;
@@ -438,7 +442,7 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
     }
   ls = ls + __shfl_xor(ls, 16);
   ls = ls + __shfl_xor(ls, 32);
-  if (g == 0 && lo < G) {
+  if (g == 0 && lo < G && !accumulate) {
     rec[G * kD + lo] = mx;
     rec[G * kD + G + lo] = ls;
   }
@@ -499,14 +503,44 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
     wave_lds_sync();  // the reads of this half complete before the next half is written
   }
   // acc[d][r]: head 4g + r, dim 16d + lo
+  if (!accumulate) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * g + r;
+      if (h < G) {
+#pragma unroll
+        for (int d = 0; d < 8; ++d) rec[h * kD + 16 * d + lo] = acc[d][r];
+      }
+    }
+    return;
+  }
+  // fold into the block record: the lanes of row 0 combine (m, l) of head lo
+  // and leave both scale factors in the (now unused) staging buffer
+  float* scale = reinterpret_cast<float*>(vbuf);
+  if (g == 0 && lo < G) {
+    const float mo = rec[G * kD + lo], lo_sum = rec[G * kD + G + lo];
+    const float mn = fmaxf(mo, mx);
+    const float so = mo == kNegInf ? 0.f : fast_exp2(mo - mn);
+    const float sn = mx == kNegInf ? 0.f : fast_exp2(mx - mn);
+    rec[G * kD + lo] = mn;
+    rec[G * kD + G + lo] = lo_sum * so + ls * sn;
+    scale[lo] = so;
+    scale[G + lo] = sn;
+  }
+  wave_lds_sync();
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int h = 4 * g + r;
     if (h < G) {
+      const float so = scale[h], sn = scale[G + h];
 #pragma unroll
-      for (int d = 0; d < 8; ++d) rec[h * kD + 16 * d + lo] = acc[d][r];
+      for (int d = 0; d < 8; ++d) {
+        float* x = rec + h * kD + 16 * d + lo;
+        *x = *x * so + acc[d][r] * sn;
+      }
     }
   }
+  wave_lds_sync();  // the scale factors are read before the buffer is reused
 }
 
 // ---- phase 2 helpers ----------------------------------------------------------
@@ -733,10 +767,10 @@ __device__ int claim_finish(const KernelParams& P, int x, uint64_t v, int lane) 
   return __builtin_amdgcn_readfirstlane(q);
 }
 
-// Phase 2 for one chunk (resolver wavefront).  `tiles` holds the chunk's tile
-// records, `aggbuf` the loaders' partial aggregates (nagg of them).
+// Phase 2 for one chunk (resolver wavefront).  `blocks` holds the chunk's
+// block records, `aggbuf` the loaders' partial aggregates (nagg of them).
 template <int G>
-__device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* tiles,
+__device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* blocks,
                               const float* aggbuf, int nagg, int lane) {
   constexpr int REC = Cfg<G>::REC;
   const GroupInfo gi = group_info(P, gidx);
@@ -744,14 +778,13 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
   const int C = P.chunk_blocks;
   const int t0 = k * C;
   const int nb = min(C, T - t0);
-  const int tpb = P.tiles_per_block;
   const __amdgpu_buffer_rsrc_t rs = record_rsrc(P, gidx);
   const int rec_agg = k * 2 * P.record_floats;          // float offsets in the group's area
   const int rec_inc = rec_agg + P.record_floats;
   int32_t* stab_me = P.stab + ((int64_t)gidx * P.max_chunks + k) * 8;
 
   // chunk aggregate: w0 (+) (w1 (+) w2) over the loaders' partials, or a
-  // left fold over the tiles when the partials did not fit in LDS
+  // left fold over the blocks when the partials did not fit in LDS
   State<G> agg;
   if (nagg == kLoaders) {
     State<G> a1, a2;
@@ -763,8 +796,8 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
   } else {
     State<G> t;
     state_clear<G>(agg);
-    for (int ti = 0; ti < nb * tpb; ++ti) {
-      read_tile<G>(tiles + ti * REC, t, lane);
+    for (int i = 0; i < nb; ++i) {
+      read_tile<G>(blocks + i * REC, t, lane);
       merge<G, false>(agg, t);
     }
   }
@@ -843,12 +876,8 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
         for (int kk = 0; kk < HPL; ++kk) pdd[u][kk] = pod[u][kk] = pn1[u][kk] = 0.f;
         const int i = i0 + u;
         if (i < nb) {
-          State<G> blkst, t;
-          read_tile<G>(tiles + (i * tpb) * REC, blkst, lane);
-          for (int jj = 1; jj < tpb; ++jj) {
-            read_tile<G>(tiles + (i * tpb + jj) * REC, t, lane);
-            merge<G, false>(blkst, t);
-          }
+          State<G> blkst;
+          read_tile<G>(blocks + i * REC, blkst, lane);
           float old_o[HPL][8];
 #pragma unroll
           for (int kk = 0; kk < HPL; ++kk)
@@ -869,7 +898,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
             pod[u][kk] = od;
             pn1[u][kk] = n1;
           }
-          write_state<G>(tiles + i * tpb * REC, s, lane);   // o(t) after block i, for the output
+          write_state<G>(blocks + i * REC, s, lane);   // o(t) after block i, for the output
         }
       }
       if (incl_pending) raise_inclusive();
@@ -984,11 +1013,11 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* til
       __hip_atomic_store(P.stop_word + gidx, (P.epoch << kQueueBits) | (uint64_t)k, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     State<G> s;
-    read_state<G>(tiles + (y.stop_t - 1 - t0) * tpb * REC, s, lane);
+    read_state<G>(blocks + (y.stop_t - 1 - t0) * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, y.stop_t, lane);
   } else if (!y.stopped && k == n_chunks - 1) {
     State<G> s;
-    read_state<G>(tiles + (nb - 1) * tpb * REC, s, lane);
+    read_state<G>(blocks + (nb - 1) * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, T, lane);
   }
 }
@@ -1006,7 +1035,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   constexpr int REC = Cfg<G>::REC;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int n_groups = P.batch * P.num_kv_heads;
-  const int CT = P.chunk_tiles_lds;
+  const int CT = P.chunk_recs_lds;
   const int nagg = P.loader_partials;
   const int slot_floats = (CT + nagg) * REC;
   const int n_slots = P.n_slots;
@@ -1114,21 +1143,21 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
     const int t0 = k * P.chunk_blocks;
     const int nb = min(P.chunk_blocks, gi.T - t0);
     const int tpb = P.tiles_per_block;
-    const int ntiles = nb * tpb;
-    float* tiles = smem + slot * slot_floats;
+    float* blocks = smem + slot * slot_floats;
     bool aborted = false;
     {
       bf16x8 qa[4];
       load_q<G>(P, gi.b, gi.kvh, lane, qa);
-      // the block list entry and the pages of every tile this wave streams,
-      // fetched together once per chunk: lane 4m + n covers 16-token group n
-      // of the wave's m-th tile (at most 16 tiles per wave)
+      // This wave streams blocks lw, lw + 3, ... of the chunk, each as its
+      // tpb tiles in order.  The block list entry and the pages of all its
+      // tiles are fetched together once per chunk: lane 4m + n covers
+      // 16-token group n of the wave's m-th tile (at most 16 tiles per wave).
+      const int n_my = lw < nb ? (nb - lw + kLoaders - 1) / kLoaders * tpb : 0;
       int my_tok0 = 0x7fffffff, my_page = 0;
       {
         const int m = lane >> 2, n = lane & 3;
-        const int ti = lw + kLoaders * m;
-        if (ti < ntiles) {
-          const int i = ti / tpb, j = ti - i * tpb;
+        if (m < n_my) {
+          const int i = lw + kLoaders * (m / tpb), j = m % tpb;
           const int step = t0 + i;
           int blk;
           if (gi.list) {
@@ -1141,14 +1170,15 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
           if (my_tok0 < gi.L) my_page = clamp_page(P, gi.b, min(my_tok0 + 16 * n, gi.L - 1));
         }
       }
-      for (int ti = lw, m = 0; ti < ntiles; ti += kLoaders, ++m) {
+      for (int m = 0; m < n_my; ++m) {
+        const int i = lw + kLoaders * (m / tpb), j = m % tpb;
         // a stop announced by an earlier chunk makes this chunk's work moot;
         // the flag read here completes while the tile's loads are in flight
         const uint64_t sw = ld_relaxed(P.stop_word + gidx);
         const int tok0 = __builtin_amdgcn_readlane(my_tok0, 4 * m);
         const int pg[4] = {__builtin_amdgcn_readlane(my_page, 4 * m), __builtin_amdgcn_readlane(my_page, 4 * m + 1),
                            __builtin_amdgcn_readlane(my_page, 4 * m + 2), __builtin_amdgcn_readlane(my_page, 4 * m + 3)};
-        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, vbuf, tiles + ti * REC);
+        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, vbuf, blocks + i * REC, j > 0);
         if (stop_word_before(sw, P.epoch, k)) {
           aborted = true;
           break;
@@ -1159,14 +1189,14 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
     if (aborted) {
       if (lane == 0) lds_st(&s_meta[slot][kMetaAbort], 1);
     } else if (nagg == kLoaders) {
-      // this loader's tiles folded in tile order: a partial aggregate
+      // this loader's blocks folded in order: a partial aggregate
       State<G> wagg, t;
       state_clear<G>(wagg);
-      for (int ti = lw; ti < ntiles; ti += kLoaders) {
-        read_tile<G>(tiles + ti * REC, t, lane);
+      for (int i = lw; i < nb; i += kLoaders) {
+        read_tile<G>(blocks + i * REC, t, lane);
         merge<G, false>(wagg, t);
       }
-      write_state<G>(tiles + CT * REC + lw * REC, wagg, lane);
+      write_state<G>(blocks + CT * REC + lw * REC, wagg, lane);
     }
     wave_lds_sync();
     if (lane == 0) {
