@@ -141,7 +141,7 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     // (a third buffer was measured: it lets loaders run further past a
     // stop and gains nothing elsewhere)
     p->slots = 2;
-    p->lds_bytes = lds_for(C * tpb, partials, p->slots);
+    p->lds_bytes = lds_for(C, partials, p->slots);
 
     art::WorkspaceLayout& w = p->ws;
     size_t off = 0;

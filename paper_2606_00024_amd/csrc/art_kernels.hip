@@ -1223,7 +1223,11 @@ int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, art_decode_kernel<G>, kThreads, plan.lds_bytes);
   if (e != hipSuccess) return (int)e;
   if (per_cu < 1) per_cu = 1;
-  const int64_t grid = min(work, (int64_t)cus * per_cu);
+  // As many workgroups as the chip holds, but at most 32 per group (and
+  // never fewer than one per CU): beyond that, a few long traversals gain
+  // nothing but reads past their stops.
+  const int64_t per_groups = max((int64_t)cus, (int64_t)32 * plan.n_groups);
+  const int64_t grid = min(work, min((int64_t)cus * per_cu, per_groups));
   hipLaunchKernelGGL(art_decode_kernel<G>, dim3((unsigned)grid), dim3(kThreads),
                      plan.lds_bytes, stream, params);
   return (int)hipGetLastError();
