@@ -665,27 +665,37 @@ struct GroupInfo {
 
 // Traversal of group gidx (indices are clamped: malformed input never makes
 // a kernel read outside the arrays the shape describes).
-__device__ __forceinline__ GroupInfo group_info(const KernelParams& P, int gidx) {
+// From the raw sequence length and list length of the group (the list
+// length is ignored for dense traversals).
+__device__ __forceinline__ GroupInfo group_info_raw(const KernelParams& P, int gidx, int L_raw, int T_raw) {
   GroupInfo g;
   g.b = gidx / P.num_kv_heads;
   g.kvh = gidx - g.b * P.num_kv_heads;
   const int64_t cap = (int64_t)P.max_pages << P.page_shift;
-  int L = P.seq_lens[g.b];
-  L = L < 0 ? 0 : (int)min((int64_t)L, cap);
+  const int L = L_raw < 0 ? 0 : (int)min((int64_t)L_raw, cap);
   g.L = L;
   g.nblk = (L + P.block_size - 1) / P.block_size;
   g.list = nullptr;
   int T = g.nblk;
   if (P.block_list) {
     const int row = P.list_per_head ? gidx : g.b;
-    T = P.block_list_len[row];
-    T = T < 0 ? 0 : min(T, P.max_list);
+    T = T_raw < 0 ? 0 : min(T_raw, P.max_list);
     g.list = P.block_list + (int64_t)row * P.max_list;
   }
   if (g.nblk == 0) T = 0;
   g.T = min(T, P.t_cap);
   g.n_chunks = (g.T + P.chunk_blocks - 1) / P.chunk_blocks;
   return g;
+}
+
+__device__ __forceinline__ int raw_list_len(const KernelParams& P, int gidx) {
+  if (!P.block_list) return 0;
+  const int b = gidx / P.num_kv_heads;
+  return P.block_list_len[P.list_per_head ? gidx : b];
+}
+
+__device__ __forceinline__ GroupInfo group_info(const KernelParams& P, int gidx) {
+  return group_info_raw(P, gidx, P.seq_lens[gidx / P.num_kv_heads], raw_list_len(P, gidx));
 }
 
 template <int G>
@@ -704,6 +714,7 @@ constexpr int kMaxSlots = 3;           // chunk buffers in LDS (the plan picks 2
 enum SlotState : int { kSlotFree = 0, kSlotLoading = 1, kSlotReady = 2, kSlotEnd = 3 };
 // slot metadata words
 constexpr int kMetaSeq = 0, kMetaState = 1, kMetaGroup = 2, kMetaChunk = 3, kMetaDone = 4, kMetaAbort = 5;
+constexpr int kMetaLen = 6, kMetaListLen = 7;  // raw seq_len and list length of the group
 
 __device__ __forceinline__ int lds_ld(const int* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -770,10 +781,9 @@ __device__ int claim_finish(const KernelParams& P, int x, uint64_t v, int lane) 
 // Phase 2 for one chunk (resolver wavefront).  `blocks` holds the chunk's
 // block records, `aggbuf` the loaders' partial aggregates (nagg of them).
 template <int G>
-__device__ void resolve_chunk(const KernelParams& P, int gidx, int k, float* blocks,
-                              const float* aggbuf, int nagg, int lane) {
+__device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const GroupInfo& gi,
+                              float* blocks, const float* aggbuf, int nagg, int lane) {
   constexpr int REC = Cfg<G>::REC;
-  const GroupInfo gi = group_info(P, gidx);
   const int b = gi.b, kvh = gi.kvh, T = gi.T, n_chunks = gi.n_chunks;
   const int C = P.chunk_blocks;
   const int t0 = k * C;
@@ -1065,7 +1075,9 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       const int k = lds_ld(&s_meta[slot][kMetaChunk]);
       if (!lds_ld(&s_meta[slot][kMetaAbort])) {
         float* base = smem + slot * slot_floats;
-        resolve_chunk<G>(P, gidx, k, base, base + CT * REC, nagg, lane);
+        const GroupInfo gi = group_info_raw(P, gidx, lds_ld(&s_meta[slot][kMetaLen]),
+                                            lds_ld(&s_meta[slot][kMetaListLen]));
+        resolve_chunk<G>(P, gidx, k, gi, base, base + CT * REC, nagg, lane);
       }
       wave_lds_sync();
       if (lane == 0) lds_st(&s_meta[slot][kMetaState], kSlotFree);
@@ -1093,7 +1105,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         }
         __builtin_amdgcn_s_sleep(1);
       }
-      int gsel = -1, ksel = -1;
+      int gsel = -1, ksel = -1, len_sel = 0, list_sel = 0;
       while (!gave_up && used_up != kAllUsedUp) {
         const int nx = (n_groups - qx + kQueues - 1) / kQueues;  // groups in queue qx
         const int i = claim_finish(P, qx, claim_issue(P, qx, lane), lane);
@@ -1103,19 +1115,27 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
           continue;
         }
         const int g = qx + kQueues * (i % nx), kh = i / nx;
-        const GroupInfo gi = group_info(P, g);
+        // the group's lengths and stop word in one round trip
+        const int L_raw = P.seq_lens[g / P.num_kv_heads];
+        const int T_raw = raw_list_len(P, g);
+        const uint64_t sw = ld_relaxed(P.stop_word + g);
+        const GroupInfo gi = group_info_raw(P, g, L_raw, T_raw);
         if (gi.n_chunks == 0) {
           if (kh == 0) write_empty_wave<G>(P, gi.b, gi.kvh, lane);
           continue;
         }
-        if (kh >= gi.n_chunks || stop_announced_before(P, g, kh)) continue;
+        if (kh >= gi.n_chunks || stop_word_before(sw, P.epoch, kh)) continue;
         gsel = g;
         ksel = kh;
+        len_sel = L_raw;
+        list_sel = T_raw;
         break;
       }
       if (lane == 0) {
         lds_st(&s_meta[slot][kMetaGroup], gsel);
         lds_st(&s_meta[slot][kMetaChunk], ksel);
+        lds_st(&s_meta[slot][kMetaLen], len_sel);
+        lds_st(&s_meta[slot][kMetaListLen], list_sel);
         lds_st(&s_meta[slot][kMetaDone], 0);
         lds_st(&s_meta[slot][kMetaAbort], 0);
       }
@@ -1139,7 +1159,8 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
     if (st == kSlotEnd) return;
     const int gidx = lds_ld(&s_meta[slot][kMetaGroup]);
     const int k = lds_ld(&s_meta[slot][kMetaChunk]);
-    const GroupInfo gi = group_info(P, gidx);
+    const GroupInfo gi = group_info_raw(P, gidx, lds_ld(&s_meta[slot][kMetaLen]),
+                                        lds_ld(&s_meta[slot][kMetaListLen]));
     const int t0 = k * P.chunk_blocks;
     const int nb = min(P.chunk_blocks, gi.T - t0);
     const int tpb = P.tiles_per_block;
