@@ -72,8 +72,10 @@ typedef enum { ART_OUT_F32 = 0, ART_OUT_BF16 = 1 } art_out_dtype;
 /*
  * Problem shape.  Element strides are in elements (bf16); the head_dim
  * stride is 1.  Supported: head_dim == 128; g = num_q_heads / num_kv_heads in
- * {1, 2, 4, 8, 16}; block_size a multiple of 64; page_size a power of two
- * >= 16.  Anything else returns ART_ERR_UNSUPPORTED.
+ * {1, 2, 4, 8, 16}; block_size a multiple of 64 of at most 1024 tokens;
+ * page_size a power of two >= 16; traversals (max_pages_per_seq * page_size
+ * / block_size, and max_blocks_per_list) shorter than 2^19 blocks.  Anything
+ * else returns ART_ERR_UNSUPPORTED.
  */
 typedef struct {
     int32_t batch;

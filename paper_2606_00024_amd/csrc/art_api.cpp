@@ -87,7 +87,8 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     const int64_t t_dense = (cap_tokens + s->block_size - 1) / s->block_size;
     int64_t t_cap = t_dense > s->max_blocks_per_list ? t_dense : s->max_blocks_per_list;
     if (t_cap < 1) t_cap = 1;
-    if (t_cap > INT32_MAX / 2) return ART_ERR_UNSUPPORTED;
+    // stability runs travel in 19 bits of a flag word
+    if (t_cap >= (int64_t(1) << 19)) return ART_ERR_UNSUPPORTED;
     const int64_t n_groups = (int64_t)s->batch * s->num_kv_heads;
 
     // LDS of a workgroup: two or three chunk buffers of C*tpb tile records
@@ -149,7 +150,6 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     w.queue_off = off;      off = align_up(off + 8 * art::kQueueStride * art::kQueues);
     w.stop_off = off;       off = align_up(off + 8 * (size_t)n_groups);
     w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
-    w.stab_off = off;       off = align_up(off + 32 * (size_t)n_groups * max_chunks);
     w.records_off = off;    off = align_up(off + (size_t)n_groups * max_chunks * 2 * p->record_floats * 4);
     // one group's records are addressed with 32-bit byte offsets
     if ((int64_t)max_chunks * 2 * p->record_floats * 4 > INT32_MAX) return ART_ERR_UNSUPPORTED;
@@ -264,7 +264,6 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.queue = reinterpret_cast<uint64_t*>(ws + plan.ws.queue_off);
     k.stop_word = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_off);
     k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
-    k.stab = reinterpret_cast<int32_t*>(ws + plan.ws.stab_off);
     k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
     k.epoch = next_epoch();
     k.spin_limit = kSpinLimit;

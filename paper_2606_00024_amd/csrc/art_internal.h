@@ -24,8 +24,9 @@ constexpr int64_t kQueueSlack = 1 << 16;
 constexpr int kQueues = 8;
 constexpr int kQueueStride = 32;  // uint64 words between queue words
 
-// Progress of one chunk, published in the low 3 bits of its flag word (the
-// rest of the word holds the call's epoch).  States only ever increase.
+// Progress of one chunk, published in bits 20..22 of its flag word (the
+// call's epoch is in bits 24..63, bits 0..19 carry the stability summary or
+// state).  States only ever increase.
 enum ChunkState : uint32_t {
     kNone = 0,
     kAggregate = 1,      // softmax aggregate of the chunk's own blocks
@@ -39,8 +40,7 @@ struct WorkspaceLayout {
     size_t error_off;        // uint32 error word
     size_t queue_off;        // kQueues work-queue words (one per 256 bytes): epoch << 24 | next index
     size_t stop_off;         // uint64 [groups] announced stop: epoch << 24 | chunk
-    size_t flags_off;        // uint64 [groups][max_chunks]
-    size_t stab_off;         // int32 [groups][max_chunks][8]
+    size_t flags_off;        // uint64 [groups][max_chunks]: epoch << 24 | state << 20 | payload
     size_t records_off;      // float [groups][max_chunks][2][record_floats]
     size_t total;
 };
@@ -91,7 +91,6 @@ struct KernelParams {
     uint64_t* queue;
     uint64_t* stop_word;
     uint64_t* flags;
-    int32_t* stab;
     float* records;
     uint64_t epoch;          // unique per call; tags every flag it writes
     uint32_t spin_limit;     // polls before a wait gives up

@@ -157,9 +157,16 @@ __device__ __forceinline__ void stores_complete() {
 }
 __device__ __forceinline__ void compiler_fence() { __asm__ __volatile__("" ::: "memory"); }
 
-__device__ __forceinline__ uint32_t flag_state(uint64_t v, uint64_t epoch) {
-  return (v >> 3) == epoch ? (uint32_t)(v & 7u) : 0u;
+// Flag words: epoch << 24 | state << 20 | payload (20 bits).  The stability
+// states carry their data in the payload, so that they are published with a
+// single store and read with the flag itself.
+__device__ __forceinline__ uint64_t make_flag(uint64_t epoch, uint32_t state, uint32_t payload) {
+  return (epoch << 24) | ((uint64_t)state << 20) | (uint64_t)payload;
 }
+__device__ __forceinline__ uint32_t flag_state(uint64_t v, uint64_t epoch) {
+  return (v >> 24) == epoch ? (uint32_t)((v >> 20) & 7u) : 0u;
+}
+__device__ __forceinline__ uint32_t flag_payload(uint64_t v) { return (uint32_t)(v & 0xfffffu); }
 
 template <int G>
 struct Cfg {
@@ -557,6 +564,23 @@ struct StabState {     // after a prefix of chunks
   int32_t pad;
 };
 
+// Payloads: a summary packs lead, trail, len (each <= 16) and fis + 1 in
+// five bits each; a stability state packs `stopped` (bit 19) and the run
+// (19 bits; traversals are shorter than 2^19 blocks, so it is exact).
+__device__ __forceinline__ uint32_t pack_summary(const StabSummary& y) {
+  return (uint32_t)y.lead | ((uint32_t)y.trail << 5) | ((uint32_t)y.len << 10) | ((uint32_t)(y.fis + 1) << 15);
+}
+__device__ __forceinline__ StabSummary unpack_summary(uint32_t p) {
+  return StabSummary{(int32_t)(p & 31u), (int32_t)((p >> 5) & 31u), (int32_t)((p >> 10) & 31u),
+                     (int32_t)((p >> 15) & 31u) - 1};
+}
+__device__ __forceinline__ uint32_t pack_stab(const StabState& x) {
+  return ((uint32_t)(x.stopped != 0) << 19) | ((uint32_t)x.run & 0x7ffffu);
+}
+__device__ __forceinline__ StabState unpack_stab(uint32_t p) {
+  return StabState{(int32_t)((p >> 19) & 1u), 0, (int32_t)(p & 0x7ffffu), 0};
+}
+
 __device__ __forceinline__ StabState stab_fold(StabState x, StabSummary y, int t0, int patience) {
   if (x.stopped) return x;
   StabState r = x;
@@ -613,10 +637,76 @@ __device__ int lookback_scan(const KernelParams& P, int gidx, int me, uint32_t n
   return -1;
 }
 
+// States whose data sits in the workspace records: the flag goes out once
+// the record stores have completed.
+// Stability state on entering chunk `me` of group gidx: the nearest chunk j
+// before it that published its stability state, with the summaries of the
+// chunks between folded forward (every chunk between must have published
+// its summary).  Flags are read 64 per poll, and when j lies within the
+// first 64 chunks back no further read is needed.  Returns false when a
+// stop before `me` has been announced or the spin limit is reached.
+__device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState& x, int lane) {
+  const uint64_t* flags = P.flags + (int64_t)gidx * P.max_chunks;
+  const int C = P.chunk_blocks;
+  int hi = me - 1, j = -1;
+  uint32_t it = 0;
+  while (hi >= 0) {
+    const int idx = hi - lane;
+    const uint64_t v = idx >= 0 ? ld_relaxed(flags + idx) : 0ull;
+    const uint32_t st = idx >= 0 ? flag_state(v, P.epoch) : 0u;
+    const uint64_t have_st = __ballot(idx >= 0 && st >= kStabInclusive);
+    const uint64_t have_sum = __ballot(idx < 0 || st >= kStabSummary);
+    const int first = have_st ? __ffsll((unsigned long long)have_st) - 1 : 64;
+    const uint64_t need = first >= 64 ? ~0ull : ((1ull << first) - 1ull);
+    if ((have_sum & need) == need) {
+      if (hi == me - 1 && (first < 64 || hi < 64)) {
+        // everything needed is in this first window: chunk hi - u is lane u
+        const uint32_t pl = flag_payload(v);
+        x = StabState{0, 0, 0, 0};
+        if (first < 64) x = unpack_stab(__builtin_amdgcn_readlane(pl, first));
+        const int top = first < 64 ? first : hi + 1;
+        for (int u = top - 1; u >= 0; --u)
+          x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), (hi - u) * C, P.patience);
+        return true;
+      }
+      if (first < 64) {
+        j = hi - first;
+        break;
+      }
+      hi -= 64;  // 64 summaries and no state among them: look further back
+      continue;
+    }
+    if (stop_announced_before(P, gidx, me)) return false;
+    if (++it >= P.spin_limit) {
+      __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+  // the state of chunk j (none when j = -1), then the summaries after it,
+  // 64 per read
+  x = StabState{0, 0, 0, 0};
+  if (j >= 0) x = unpack_stab(flag_payload(ld_relaxed(flags + j)));
+  for (int i0 = j + 1; i0 < me; i0 += 64) {
+    const int n = min(64, me - i0);
+    const uint32_t pl = lane < n ? flag_payload(ld_relaxed(flags + i0 + lane)) : 0u;
+    for (int u = 0; u < n; ++u)
+      x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), (i0 + u) * C, P.patience);
+  }
+  return true;
+}
+
 __device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, uint32_t state, int lane) {
   stores_complete();
   if (lane == 0)
-    __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, (P.epoch << 3) | state,
+    __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, make_flag(P.epoch, state, 0),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// States carried in the flag word itself: one store, no wait.
+__device__ __forceinline__ void publish_word(const KernelParams& P, int gidx, int k, uint32_t state,
+                                             uint32_t payload, int lane) {
+  if (lane == 0)
+    __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, make_flag(P.epoch, state, payload),
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 template <int G>
@@ -791,7 +881,6 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   const __amdgpu_buffer_rsrc_t rs = record_rsrc(P, gidx);
   const int rec_agg = k * 2 * P.record_floats;          // float offsets in the group's area
   const int rec_inc = rec_agg + P.record_floats;
-  int32_t* stab_me = P.stab + ((int64_t)gidx * P.max_chunks + k) * 8;
 
   // chunk aggregate: w0 (+) (w1 (+) w2) over the loaders' partials, or a
   // left fold over the blocks when the partials did not fit in LDS
@@ -968,60 +1057,24 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     sm.len = nb;
     sm.fis = fis;
   }
-  if (lane == 0) {
-    st_coh_i32(stab_me + 0, sm.lead);
-    st_coh_i32(stab_me + 1, sm.trail);
-    st_coh_i32(stab_me + 2, sm.len);
-    st_coh_i32(stab_me + 3, sm.fis);
-  }
-  publish(P, gidx, k, kStabSummary, lane);
+  publish_word(P, gidx, k, kStabSummary, pack_summary(sm), lane);
   // A chunk whose first block is unstable and whose own run never reaches
   // the patience cannot hold the stop, whatever run it enters with: unless
   // it is the last chunk (which writes the untruncated result) it is done.
   if (sm.lead == 0 && sm.fis < 0 && k != n_chunks - 1) return;
 
-  // entering stability state: nearest chunk with an inclusive stability
-  // state, then the summaries after it (fetched one per lane)
-  j = lookback_scan(P, gidx, k, kStabSummary, kStabInclusive, lane);
-  if (j == -2) return;
-  compiler_fence();
-  StabState x{0, 0, 0, 0};
-  if (j >= 0) {
-    const int32_t* sj = P.stab + ((int64_t)gidx * P.max_chunks + j) * 8;
-    x.stopped = ld_coh_i32(sj + 4);
-    x.stop_t = ld_coh_i32(sj + 5);
-    x.run = ld_coh_i32(sj + 6);
-  }
-  for (int i0 = j + 1; i0 < k; i0 += 64) {
-    const int n = min(64, k - i0);
-    int32_t y0 = 0, y1 = 0, y2 = 0, y3 = 0;
-    if (lane < n) {
-      const int32_t* si = P.stab + ((int64_t)gidx * P.max_chunks + i0 + lane) * 8;
-      y0 = ld_coh_i32(si + 0);
-      y1 = ld_coh_i32(si + 1);
-      y2 = ld_coh_i32(si + 2);
-      y3 = ld_coh_i32(si + 3);
-    }
-    for (int u = 0; u < n; ++u) {
-      const StabSummary y{__builtin_amdgcn_readlane(y0, u), __builtin_amdgcn_readlane(y1, u),
-                          __builtin_amdgcn_readlane(y2, u), __builtin_amdgcn_readlane(y3, u)};
-      x = stab_fold(x, y, (i0 + u) * C, P.patience);
-    }
-  }
+  // entering stability state, then this chunk's own
+  StabState x;
+  if (!stab_entering(P, gidx, k, x, lane)) return;
   const bool stopped_before = x.stopped != 0;
   const StabState y = stab_fold(x, sm, t0, P.patience);
-  if (lane == 0) {
-    st_coh_i32(stab_me + 4, y.stopped);
-    st_coh_i32(stab_me + 5, y.stop_t);
-    st_coh_i32(stab_me + 6, y.run);
-  }
-  publish(P, gidx, k, kStabInclusive, lane);
+  if (!stopped_before && y.stopped && lane == 0)  // the stop lies in this chunk: announce it at once
+    __hip_atomic_store(P.stop_word + gidx, (P.epoch << kQueueBits) | (uint64_t)k, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  publish_word(P, gidx, k, kStabInclusive, pack_stab(y), lane);
   wave_lds_sync();  // saved per-block states were written by other lanes
   if (!stopped_before && y.stopped) {
-    // the stop lies in this chunk: announce it, then write o(t*)
-    if (lane == 0)
-      __hip_atomic_store(P.stop_word + gidx, (P.epoch << kQueueBits) | (uint64_t)k, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+    // the stop lies in this chunk: write o(t*)
     State<G> s;
     read_state<G>(blocks + (y.stop_t - 1 - t0) * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, y.stop_t, lane);
