@@ -119,9 +119,11 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     if (o->chunk_blocks > 0) {
         C = o->chunk_blocks;
     } else {
-        // about 8 blocks per chunk; smaller chunks when the whole problem
-        // would not give the 256 CUs enough work
-        C = 8;
+        // up to 9 blocks per chunk, a multiple of the three loaders when the
+        // budget allows; smaller chunks when the whole problem would not
+        // give the 256 CUs enough work
+        C = c_max < 9 ? c_max : 9;
+        if (C >= 3) C -= C % 3;
         while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
         // the work list must fit a queue word
         while (C < c_max && n_groups * ((t_cap + C - 1) / C) + art::kQueueSlack >= (1 << art::kQueueBits)) C *= 2;
