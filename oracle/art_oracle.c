@@ -15,7 +15,8 @@
  *                               no exponential overflows; the coefficients
  *                               A(t-1)/A(t) and l(t)/A(t) are the same numbers.
  *   Eq. (2), Sec. 3.2 ......... d_scale = ||x(t) - x(t-1)||_2,
- *                               d_direction = 1 - cos(x(t), x(t-1)), x = o.
+ *                               d_direction = 1 - cos(x(t), x(t-1)),
+ *                               x(t) = P o(t) (the probe of Appendix A).
  *   Sec. 3.2 .................. stable iff d_scale < tau and d_direction < phi.
  *   Eq. (3) ................... c(t) = c(t-1) + 1 if stable else 0.
  *   Algorithm 1 ............... o(0) = 0, c(0) = 0; after the update of step t,
@@ -25,8 +26,12 @@
  *                               follows a supplied list of block ids.
  *
  * Readings where the paper is silent or ambiguous:
- *   R1 probe: x(t) is the whole normalised output o(t) of each query head
- *      (P = I, the "oracle detector" of Appendix B).
+ *   R1 probe: by default x(t) is the whole normalised output o(t) of each
+ *      query head (P = I, the full-output detector Appendix B compares
+ *      against).  With probe_stride s > 1, P keeps the coordinates
+ *      0, s, 2s, ... of o(t) (m = D / s): a fixed subsample spread over the
+ *      head dimension, in place of Sec. 3.2's subsample taken from the
+ *      accumulator's register layout (m = 32 there, i.e. s = 4 at D = 128).
  *   R2 o(t) is the normalised running output (Appendix A), not the
  *      unnormalised accumulator.
  *   R3 grouped-query attention: one decision per (sequence, KV head); a step is
@@ -75,6 +80,7 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
     const int g = S->num_q_heads / S->num_kv_heads;
     const int D = S->head_dim;
     const int Bk = S->block_size;
+    const int ps = O->probe_stride;
     const int L = seq_lens[b];
     const int nblk = L > 0 ? (L + Bk - 1) / Bk : 0;
     const int gi = b * S->num_kv_heads + kvh;
@@ -161,15 +167,17 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
             const double w = exp(logl - logA_new);         /* l(t) / A(t)   */
             logA[i] = logA_new;
             /* o(t) = (A(t-1) o(t-1) + l(t) u(t)) / A(t) */
+            for (int d = 0; d < D; ++d)
+                onew[i * D + d] = keep * o[i * D + d] + w * u[i * D + d];
+            /* probe coordinates of o(t) and o(t-1) (R1) */
             double ds2 = 0.0, dot = 0.0, n_new = 0.0, n_old = 0.0;
-            for (int d = 0; d < D; ++d) {
-                const double x = keep * o[i * D + d] + w * u[i * D + d];
-                onew[i * D + d] = x;
-                const double diff = x - o[i * D + d];
+            for (int d = 0; d < D; d += ps) {
+                const double x = onew[i * D + d], x0 = o[i * D + d];
+                const double diff = x - x0;
                 ds2 += diff * diff;
-                dot += x * o[i * D + d];
+                dot += x * x0;
                 n_new += x * x;
-                n_old += o[i * D + d] * o[i * D + d];
+                n_old += x0 * x0;
             }
             /* Eq. (2) */
             const double d_scale = sqrt(ds2);
@@ -244,7 +252,8 @@ int artref_decode(const artref_shape* S, const artref_opts* O,
         return ARTREF_ERR_ARG;
     if (S->batch < 0 || S->num_kv_heads <= 0 || S->num_q_heads <= 0 ||
         S->num_q_heads % S->num_kv_heads || S->head_dim <= 0 || S->block_size <= 0 ||
-        S->page_size <= 0 || O->patience < 1 || (block_list && !block_list_len) ||
+        S->page_size <= 0 || O->patience < 1 || O->probe_stride < 1 ||
+        S->head_dim % O->probe_stride || (block_list && !block_list_len) ||
         (!block_list && block_list_len) || (trace && trace_steps < 0))
         return ARTREF_ERR_ARG;
     for (int b = 0; b < S->batch; ++b)

@@ -13,8 +13,9 @@
  *     importance-first through an index mapping);
  *   - for t = 1..T the block-streaming softmax of Sec. 3.1 in the normalised
  *     form of Appendix A: o(t) = (A(t-1) o(t-1) + l(t) u(t)) / A(t);
- *   - the stability metrics of Eq. (2): d_scale = ||o(t) - o(t-1)||_2 and
- *     d_direction = 1 - cos(o(t), o(t-1)) with o(0) = 0 (Algorithm 1);
+ *   - the stability metrics of Eq. (2) on the probe x(t) = P o(t):
+ *     d_scale = ||x(t) - x(t-1)||_2 and d_direction = 1 - cos(x(t), x(t-1))
+ *     with o(0) = 0 (Algorithm 1);
  *   - the patience counter of Eq. (3) and the break of Algorithm 1;
  *   - out = o(t*), lse = ln A(t*), stop_block = t*.
  * Readings where the paper is silent are listed in the .c file header.
@@ -49,6 +50,9 @@ typedef struct {
     double phi;          /* d_direction threshold (strict <) */
     int32_t patience;    /* p >= 1 */
     int32_t dense_order; /* 0: recency-first, 1: forward; ignored with a list */
+    int32_t probe_stride; /* probe x = P o (Sec. 3.2, Appendix A): 1 = the whole
+                             output (P = I); s > 1 (s divides head_dim) = the
+                             coordinates 0, s, 2s, ... of o (m = head_dim / s) */
 } artref_opts;
 
 enum {

@@ -124,10 +124,14 @@ def step_metrics(o_new: np.ndarray, o_old: np.ndarray):
 
 
 def stop_from_trajectory(o_traj, tau: float, phi: float, patience: int,
-                         use_scale=True, use_direction=True):
+                         use_scale=True, use_direction=True, probe=None):
     """Apply Sec. 3.2 / Eq. (3) / Algorithm 1 to a trajectory o(0..T).
+    ``probe`` is an optional linear map P (an m x D matrix): the metrics are
+    then taken on x(t) = P o(t) (Appendix A) instead of o(t).
     Returns (t_star, [(d_scale, d_direction) per step])."""
     T = len(o_traj) - 1
+    if probe is not None:
+        o_traj = [o @ np.asarray(probe).T for o in o_traj]
     c = 0
     mets = []
     for t in range(1, T + 1):

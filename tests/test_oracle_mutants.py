@@ -24,8 +24,8 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 MUTANTS = {
     "recurrence_drops_old_weight": (
-        "const double x = keep * o[i * D + d] + w * u[i * D + d];",
-        "const double x = o[i * D + d] + w * u[i * D + d];"),
+        "onew[i * D + d] = keep * o[i * D + d] + w * u[i * D + d];",
+        "onew[i * D + d] = o[i * D + d] + w * u[i * D + d];"),
     "value_index_reversed": (
         "u[i * D + d] += e * bf16_to_double(vj[d]);",
         "u[i * D + d] += e * bf16_to_double(vj[D - 1 - d]);"),
@@ -110,8 +110,68 @@ def _battery(lib) -> list[str]:
     return sorted(set(fails))
 
 
+PROBE_MUTANTS = {
+    "probe_stride_ignored": ("for (int d = 0; d < D; d += ps) {", "for (int d = 0; d < D; d += 1) {"),
+    "probe_offset_shifted": ("for (int d = 0; d < D; d += ps) {",
+                             "for (int d = ps - 1; d < D; d += ps) {"),
+    "probe_on_new_only": ("const double x = onew[i * D + d], x0 = o[i * D + d];",
+                          "const double x = onew[i * D + d], x0 = o[i * D + (d ^ 1)];"),
+}
+
+
+def _probe_battery(lib) -> list[str]:
+    """Brute force with an explicit selection matrix, plus the closed forms
+    of tests/test_oracle_probe.py, at stride 4."""
+    fails = []
+    s_ = 4
+    wl = small_workload(311, batch=1, kv_heads=2, group=4, seq_len=1000, page_size=16)
+    sp = wl.spec
+    scale = float32(sp.softmax_scale)
+    P = np.eye(128)[::s_]
+    for tau, phi, p in ((0.05, 1e-3, 2), (0.02, 1e-2, 3)):
+        T = max(max(x) for x in wl.traversal_lengths())
+        r = oracle.decode_workload(wl, tau=tau, phi=phi, patience=p, trace_steps=T,
+                                   probe_stride=s_, _lib=lib)
+        for b in range(sp.batch):
+            for h in range(sp.num_kv_heads):
+                grp = Group(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens, b, h,
+                            sp.block_size, sp.dense_order, None, None)
+                traj = prefix_outputs(grp, scale)["o"]
+                ts, mets = stop_from_trajectory(traj, float32(tau), float32(phi), p, probe=P)
+                if int(r["stop"][b, h]) != ts:
+                    fails.append("probe_stop")
+                for t in range(1, min(ts, int(r["stop"][b, h])) + 1):
+                    ds, dr = mets[t - 1]
+                    tr = r["trace"][b, h, t - 1]
+                    if not (np.allclose(tr[:, 0], ds, rtol=1e-9, atol=1e-13) and
+                            np.allclose(tr[:, 1], dr, rtol=1e-6, atol=1e-12, equal_nan=True)):
+                        fails.append("probe_trace")
+                        break
+    rng = np.random.default_rng(5)
+    off = rng.standard_normal(128)
+    off[::s_] = 0.0
+    q, k, v, pt, sl = uniform_key_case([off] * 10)
+    k = k + 0.5  # non-uniform keys are not needed: values are constant
+    r = oracle.decode(q, k, v, pt, sl, block_size=64, scale=0.088, tau=1e-6, phi=1e-9,
+                      patience=3, probe_stride=s_, _lib=lib)
+    if int(r["stop"][0, 0]) != 10:
+        fails.append("probe_blind_off_probe")
+    return sorted(set(fails))
+
+
 def test_battery_passes_on_the_real_oracle():
     assert _battery(None) == []
+    assert _probe_battery(None) == []
+
+
+@pytest.mark.parametrize("name", sorted(PROBE_MUTANTS))
+def test_planted_probe_mistake_is_caught(name, tmp_path):
+    old, new = PROBE_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    path = oracle.build_variant(src.replace(old, new), str(tmp_path / f"{name}.so"))
+    fails = _probe_battery(oracle.load_library(path))
+    assert fails, f"planted mistake '{name}' passed every probe pin"
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
