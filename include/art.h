@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 1
+#define ART_ABI_VERSION 2
 
 typedef enum {
     ART_OK = 0,
@@ -102,6 +102,15 @@ typedef struct {
  * thresholds); 1..16 asks for that many blocks per chunk (capped at what
  * the shared-memory budget holds for the shape).  The chunking changes
  * rounding only.
+ *
+ * probe_stride chooses the probe x(t) = P o(t) that the stability test of
+ * Eq. (2) looks at (Sec. 3.2; P is the linear map of Appendix A): 0 or 1
+ * tests the whole normalised output of every query head (P = I); s > 1,
+ * a power of two dividing head_dim, tests only its coordinates 0, s, 2s,
+ * ... (m =
+ * head_dim / s values spread over the head dimension, a fixed stand-in for
+ * the subsample Sec. 3.2 takes from the accumulator's register layout; the
+ * paper's m = 32 is s = 4).  The output and lse are always the full ones.
  */
 typedef struct {
     float softmax_scale;           /* usually 1/sqrt(head_dim) (Eq. 1) */
@@ -111,6 +120,7 @@ typedef struct {
     int32_t dense_order;           /* art_order; ignored when block_list != NULL */
     int32_t out_dtype;             /* art_out_dtype */
     int32_t chunk_blocks;          /* 0 = automatic */
+    int32_t probe_stride;          /* 0 or 1 = whole output; s > 1 = every s-th coordinate */
 } art_decode_opts;
 
 /* Version of this ABI (ART_ABI_VERSION). */

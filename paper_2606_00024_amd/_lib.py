@@ -35,11 +35,15 @@ class DecodeShape(ctypes.Structure):
             "v_stride_page", "v_stride_head", "v_stride_token")]
 
 
+# ART_ABI_VERSION of include/art.h that these structure layouts follow
+ABI_VERSION = 2
+
+
 class DecodeOpts(ctypes.Structure):
     _fields_ = [("softmax_scale", ctypes.c_float), ("tau", ctypes.c_float),
                 ("phi", ctypes.c_float), ("patience", ctypes.c_int32),
                 ("dense_order", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
-                ("chunk_blocks", ctypes.c_int32)]
+                ("chunk_blocks", ctypes.c_int32), ("probe_stride", ctypes.c_int32)]
 
 
 class ArtError(RuntimeError):
@@ -82,6 +86,10 @@ def load() -> ctypes.CDLL:
             ctypes.POINTER(ctypes.c_int64), i32p]
         lib.art_workspace_status.restype = ctypes.c_int
         lib.art_workspace_status.argtypes = [vp, ctypes.c_size_t, vp, i32p]
+        got = int(lib.art_abi_version())
+        if got != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {got}, this binding needs "
+                               f"{ABI_VERSION}: rebuild it")
         _lib = lib
     return _lib
 

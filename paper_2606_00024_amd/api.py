@@ -51,13 +51,14 @@ def make_shape(q, k_cache, v_cache, page_table, *, block_size: int, block_list=N
 
 
 def make_opts(*, softmax_scale: float, tau: float, phi: float, patience: int,
-              dense_order: int = 0, out_dtype=torch.float32, chunk_blocks: int = 0) -> DecodeOpts:
+              dense_order: int = 0, out_dtype=torch.float32, chunk_blocks: int = 0,
+              probe_stride: int = 1) -> DecodeOpts:
     od = _lib.OUT_BF16 if out_dtype == torch.bfloat16 else _lib.OUT_F32
     if out_dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_dtype must be float32 or bfloat16")
     return DecodeOpts(softmax_scale=float(softmax_scale), tau=float(tau), phi=float(phi),
                       patience=int(patience), dense_order=int(dense_order), out_dtype=od,
-                      chunk_blocks=int(chunk_blocks))
+                      chunk_blocks=int(chunk_blocks), probe_stride=int(probe_stride))
 
 
 def workspace_bytes(shape: DecodeShape, opts: DecodeOpts) -> int:
@@ -90,7 +91,8 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                      block_list: Optional[torch.Tensor] = None,
                      block_list_len: Optional[torch.Tensor] = None,
                      list_per_head: bool = True, out_dtype=torch.float32,
-                     chunk_blocks: int = 0, workspace: Optional[torch.Tensor] = None,
+                     chunk_blocks: int = 0, probe_stride: int = 1,
+                     workspace: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      stop_block: Optional[torch.Tensor] = None):
     """ART decode attention on the current stream.
@@ -98,6 +100,8 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     Returns (out [B][Hq][D] out_dtype, lse [B][Hq] fp32, stop_block [B][Hkv]
     int32).  ``workspace`` (uint8, zero-filled before its first use, e.g. by
     ``new_workspace``) defaults to a per-(device, stream) cached buffer.
+    ``probe_stride`` s > 1 makes the stability test look at every s-th
+    coordinate of each head's output only (Sec. 3.2's subsampled probe).
     """
     _require_cuda(q, "q", torch.bfloat16)
     _require_cuda(k_cache, "k_cache", torch.bfloat16)
@@ -120,7 +124,8 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     shape = make_shape(q, k_cache, v_cache, page_table, block_size=block_size,
                        block_list=block_list, list_per_head=list_per_head)
     opts = make_opts(softmax_scale=softmax_scale, tau=tau, phi=phi, patience=patience,
-                     dense_order=dense_order, out_dtype=out_dtype, chunk_blocks=chunk_blocks)
+                     dense_order=dense_order, out_dtype=out_dtype, chunk_blocks=chunk_blocks,
+                     probe_stride=probe_stride)
     dev = q.device
     if out is None:
         out = torch.empty((B, Hq, D), dtype=out_dtype, device=dev)

@@ -69,6 +69,7 @@ struct KernelParams {
     float scale_log2;        // softmax_scale * log2(e): scores kept in base 2
     float tau, phi;
     int32_t patience, dense_order, out_bf16;
+    int32_t probe_stride;    // the stability test sees coordinates 0, s, 2s, ... (1 = all)
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
     int32_t work_chunks;     // chunk rows of the work list (<= max_chunks)

@@ -958,13 +958,21 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   uint32_t stable_bits = 0;
   {
     State<G> s = pre;
-    // |o|^2 per head slot of the state before the next block
+    // Probe weights (Sec. 3.2, x = P o): 1 on the coordinates the test looks
+    // at (every probe_stride-th of the head dimension), 0 elsewhere.  This
+    // lane holds coordinates 8*(lane&15) .. +7.  Multiplying by 1 is exact,
+    // so the whole-output test is unchanged bit for bit.
+    float pw[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      pw[e] = ((8 * (lane & 15) + e) & (P.probe_stride - 1)) == 0 ? 1.f : 0.f;
+    // |x|^2 per head slot of the state before the next block
     float n_prev[HPL];
 #pragma unroll
     for (int kk = 0; kk < HPL; ++kk) {
       float n0 = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n0);
+      for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(s.o[kk][e] * pw[e], s.o[kk][e], n0);
       n_prev[kk] = row_sum(n0);
     }
     for (int i0 = 0; i0 < nb; i0 += NB) {
@@ -989,9 +997,9 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
             float dd = 0.f, od = 0.f, n1 = 0.f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              dd = __builtin_fmaf(d[kk][e], d[kk][e], dd);
-              od = __builtin_fmaf(old_o[kk][e], d[kk][e], od);
-              n1 = __builtin_fmaf(s.o[kk][e], s.o[kk][e], n1);
+              dd = __builtin_fmaf(d[kk][e] * pw[e], d[kk][e], dd);
+              od = __builtin_fmaf(old_o[kk][e] * pw[e], d[kk][e], od);
+              n1 = __builtin_fmaf(s.o[kk][e] * pw[e], s.o[kk][e], n1);
             }
             pdd[u][kk] = dd;
             pod[u][kk] = od;
@@ -1018,7 +1026,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
         for (int kk = 0; kk < HPL; ++kk) {
           const float n0 = n_prev[kk], dd = pdd[u][kk], od = pod[u][kk], n1 = pn1[u][kk];
           n_prev[kk] = n1;
-          // Eq. (2): d_scale = |d|; d_direction = 1 - cos(o_new, o_old)
+          // Eq. (2) on the probe: d_scale = |P d|; d_direction = 1 - cos(P o_new, P o_old)
           const float d_scale = fast_sqrt(dd);
           const float nn = __fmul_rn(fast_sqrt(n1), fast_sqrt(n0));
           const float dot = __fadd_rn(n0, od);

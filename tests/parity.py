@@ -88,7 +88,7 @@ def compare_group(rep: Report, tag, out_g, lse_g, stop_g, ref_out, ref_lse, ref_
 
 
 def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=None,
-                     num_threads=0) -> Report:
+                     num_threads=0, probe_stride=1) -> Report:
     """Whole workload (small sizes): oracle on every group."""
     rep = report or Report()
     s = wl.spec
@@ -98,7 +98,8 @@ def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=No
     T = max([max(r) for r in wl.traversal_lengths()] + [1])
     do = s.dense_order if dense_order is None else dense_order
     ref = oracle.decode_workload(wl, tau=tau, phi=phi, patience=patience, dense_order=do,
-                                 trace_steps=T, num_threads=num_threads)
+                                 trace_steps=T, num_threads=num_threads,
+                                 probe_stride=probe_stride)
     for b in range(s.batch):
         for h in range(s.num_kv_heads):
             def rerun(st, b=b, h=h):
@@ -107,7 +108,8 @@ def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=No
                 fs[b, h] = st
                 m[b, h] = 1
                 r = oracle.decode_workload(wl, tau=tau, phi=phi, patience=patience,
-                                           dense_order=do, force_stop=fs, group_mask=m)
+                                           dense_order=do, force_stop=fs, group_mask=m,
+                                           probe_stride=probe_stride)
                 return r["out"][b, h * g:(h + 1) * g], r["lse"][b, h * g:(h + 1) * g]
             compare_group(rep, (b, h), out[b, h * g:(h + 1) * g].astype(np.float64),
                           lse[b, h * g:(h + 1) * g].astype(np.float64), int(stop[b, h]),
@@ -116,7 +118,8 @@ def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=No
     return rep
 
 
-def compare_sampled(wl, gpu, groups, *, tau, phi, patience, report=None, num_threads=0) -> Report:
+def compare_sampled(wl, gpu, groups, *, tau, phi, patience, report=None, num_threads=0,
+                    probe_stride=1) -> Report:
     """Full-size workloads: the oracle runs on host copies of the sampled
     groups only (workloads.group_subproblem)."""
     from paper_2606_00024_amd.workloads import group_subproblem
@@ -130,7 +133,8 @@ def compare_sampled(wl, gpu, groups, *, tau, phi, patience, report=None, num_thr
                 else -(-int(sub["seq_lens"][0]) // s.block_size))
         kw = dict(block_size=s.block_size, scale=s.softmax_scale, tau=tau, phi=phi,
                   patience=patience, dense_order=s.dense_order, block_list=sub["block_list"],
-                  block_list_len=sub["block_list_len"], num_threads=num_threads)
+                  block_list_len=sub["block_list_len"], num_threads=num_threads,
+                  probe_stride=probe_stride)
         ref = oracle.decode(sub["q"], sub["k_cache"], sub["v_cache"], sub["page_table"],
                             sub["seq_lens"], trace_steps=T, **kw)
 

@@ -37,7 +37,9 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert _lib.abi_version() == 1
+    with open(os.path.join(ROOT, "include", "art.h")) as f:
+        declared = int(re.search(r"#define ART_ABI_VERSION (\d+)", f.read()).group(1))
+    assert _lib.abi_version() == declared == _lib.ABI_VERSION
     assert _lib.status_str(0) == "ART_OK"
     assert _lib.status_str(3) == "ART_ERR_WORKSPACE_TOO_SMALL"
     assert _lib.status_str(6) == "ART_ERR_DEVICE_TIMEOUT"
@@ -89,11 +91,20 @@ def test_shape_errors(lib, kw, status):
 @pytest.mark.parametrize("kw", [
     dict(tau=float("nan")), dict(phi=float("nan")), dict(patience=0), dict(dense_order=2),
     dict(out_dtype=5), dict(chunk_blocks=-1), dict(chunk_blocks=17),
-    dict(softmax_scale=float("inf")),
+    dict(softmax_scale=float("inf")), dict(probe_stride=-1), dict(probe_stride=3),
+    dict(probe_stride=6), dict(probe_stride=256),
 ])
 def test_option_errors(lib, kw):
     n, st = _ws(_shape(), _opts(**kw))
     assert (n, st) == (0, _lib.ERR_INVALID_ARG)
+
+
+@pytest.mark.parametrize("stride", [0, 1, 2, 4, 8, 32, 128])
+def test_probe_strides_accepted(lib, stride):
+    """Every power of two dividing head_dim is a valid probe; the workspace
+    does not depend on it."""
+    n, st = _ws(_shape(), _opts(probe_stride=stride))
+    assert st == _lib.OK and n == _ws(_shape(), _opts())[0]
 
 
 def test_workspace_size_depends_on_shape_only(lib):
