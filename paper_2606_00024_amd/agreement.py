@@ -103,16 +103,24 @@ def length_sweep_specs(lengths=(1024, 2048, 4096, 8192, 32768), batch=32, seed=4
 
 
 def measure(spec, strides: Iterable[int], thresholds: Iterable[tuple], device="cuda:0",
-            seeds: Iterable[int] = (0,)) -> list[dict]:
+            seeds: Iterable[int] = (0,), rescale_tau: Iterable[bool] = (False, True)) -> list[dict]:
     """Run the GPU path with the full-output test and with each probe stride
-    on ``spec`` (once per seed offset) and classify every group."""
+    on ``spec`` (once per seed offset) and classify every group.
+
+    d_scale is an absolute norm, and the norm of m of the D coordinates of a
+    vector is about sqrt(m / D) of the whole one when its energy is spread
+    evenly; never more.  With the same tau the probe's scale test is thus
+    looser than the full output's.  ``rescale_tau`` True runs the probe with
+    tau * sqrt(m / D) instead, the matched threshold for spread increments
+    (d_direction is a ratio and keeps phi)."""
     import torch
     from dataclasses import replace
     from . import api, workloads as W
     rows = []
     strides = list(strides)
     thresholds = list(thresholds)
-    acc = {(s, thr): Agreement() for s in strides for thr in thresholds}
+    rescale_tau = list(rescale_tau)
+    acc = {(s, thr, rs): Agreement() for s in strides for thr in thresholds for rs in rescale_tau}
     for sd in seeds:
         wl = W.make_workload(replace(spec, seed=spec.seed + 1000 * sd), device=device)
         T = np.asarray(wl.traversal_lengths(), dtype=np.int64)
@@ -120,14 +128,17 @@ def measure(spec, strides: Iterable[int], thresholds: Iterable[tuple], device="c
             tau, phi, p = thr
             full = api.decode_workload(wl, tau=tau, phi=phi, patience=p)[2].cpu().numpy()
             for s in strides:
-                probe = api.decode_workload(wl, tau=tau, phi=phi, patience=p,
-                                            probe_stride=s)[2].cpu().numpy()
-                classify(probe, full, T, into=acc[(s, thr)])
+                for rs in rescale_tau:
+                    tau_p = tau * (1.0 / s) ** 0.5 if rs else tau
+                    probe = api.decode_workload(wl, tau=tau_p, phi=phi, patience=p,
+                                                probe_stride=s)[2].cpu().numpy()
+                    classify(probe, full, T, into=acc[(s, thr, rs)])
         del wl
         torch.cuda.empty_cache()
-    for (s, thr), a in acc.items():
+    for (s, thr, rs), a in acc.items():
         r = {"workload": spec.name, "probe_stride": s, "probe_dims": spec.head_dim // s,
-             "tau": thr[0], "phi": thr[1], "patience": thr[2]}
+             "tau": thr[0], "tau_probe": thr[0] * (1.0 / s) ** 0.5 if rs else thr[0],
+             "phi": thr[1], "patience": thr[2]}
         r.update(a.rates())
         rows.append(r)
     return rows
@@ -140,14 +151,15 @@ def _fmt(x, nd=2):
 
 
 def markdown(rows: list[dict]) -> str:
-    head = ("| workload | m | tau | phi | p | groups | agree % | FP % | FN % | "
+    head = ("| workload | m | tau | probe tau | phi | p | groups | agree % | FP % | FN % | "
             "delta_blk (mean ± std, n) | skipped % probe / full |\n"
-            "|---|---|---|---|---|---|---|---|---|---|---|\n")
+            "|---|---|---|---|---|---|---|---|---|---|---|---|\n")
     body = ""
     for r in rows:
         d = ("-" if r["delta_blk_mean"] is None else
              f"{r['delta_blk_mean']:.2f} ± {r['delta_blk_std']:.2f} ({r['delta_blk_n']})")
-        body += (f"| {r['workload']} | {r['probe_dims']} | {r['tau']:g} | {r['phi']:g} | "
+        body += (f"| {r['workload']} | {r['probe_dims']} | {r['tau']:g} | "
+                 f"{r.get('tau_probe', r['tau']):.3g} | {r['phi']:g} | "
                  f"{r['patience']} | {r['groups']} | {_fmt(r['agree_pct'])} | {_fmt(r['fp_pct'])} | "
                  f"{_fmt(r['fn_pct'])} | {d} | {_fmt(r['skipped_pct_probe'], 1)} / "
                  f"{_fmt(r['skipped_pct_full'], 1)} |\n")
