@@ -1101,8 +1101,11 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
 // earlier, so the launch always makes progress.
 template <int G>
 __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
-  extern __shared__ float smem[];
-  __shared__ int s_meta[kMaxSlots][8];
+  // the dynamic buffers must start 16-byte aligned (128-bit LDS accesses):
+  // the static block below is a multiple of 16 bytes
+  extern __shared__ __align__(16) float smem[];
+  __shared__ __align__(16) int s_meta[kMaxSlots][8];
+  static_assert(sizeof(int) * kMaxSlots * 8 % 16 == 0, "static LDS must keep the dynamic part aligned");
   constexpr int REC = Cfg<G>::REC;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int n_groups = P.batch * P.num_kv_heads;
