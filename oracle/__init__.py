@@ -44,13 +44,16 @@ class Opts(ctypes.Structure):
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (-O2, fp-contract off, OpenMP)."""
+    """Compile the oracle (and the traversal-list oracle, ``oracle.lists``)
+    with gcc (-O2, fp-contract off, OpenMP)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
                "-ffp-contract=off", "-Wall", "-o", tmp, _SRC, "-lm"]
         subprocess.check_call(cmd)
         os.replace(tmp, _LIB)
+    from . import lists
+    lists.build(force=force)
     return _LIB
 
 
