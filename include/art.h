@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 2
+#define ART_ABI_VERSION 3
 
 typedef enum {
     ART_OK = 0,
@@ -191,6 +191,79 @@ art_status art_validate_inputs(const art_decode_shape* shape, const art_decode_o
  */
 art_status art_workspace_status(const void* workspace, size_t workspace_bytes,
                                 hipStream_t stream, int32_t* device_status);
+
+/*
+ * Traversal lists (Sec. 3.4).  ART stops early only if the blocks that carry
+ * the attention mass come first.  For a full cache the decode call itself
+ * walks recency-first (dense_order).  For other KV policies it takes a
+ * block list.  These calls build one on the device, in the decode call's
+ * list layout (list_per_head = 1):
+ *
+ *   ART_LIST_IMPORTANCE  every block of each (sequence, KV head) gets a score.
+ *       The first `sink_blocks` blocks, and the last block when keep_last = 1,
+ *       are always kept.  Of the other blocks, the best `budget` minus (the
+ *       kept count) are added.  The list holds the kept blocks in descending
+ *       score order; equal scores put the smaller block id first.  Scores are
+ *       doubles, each sum taken over dimensions 0..127 in order from exact
+ *       products of the bf16 inputs:
+ *         ART_SCORE_KEY_NORM:    max over the block's tokens of sum_d k_d^2.
+ *         ART_SCORE_QUERY_BOUND: max over the group's query heads of
+ *                                sum_d max(q_d * min_j k_jd, q_d * max_j k_jd),
+ *                                which bounds q . k_j over the block from above.
+ *   ART_LIST_STREAMING  a cache of sink tokens plus a recent window
+ *       (pattern-based policies).  Blocks 0 .. sink_blocks-1 come first, in
+ *       increasing order, so that a stop never drops the sinks.  Then come the
+ *       `budget` most recent other blocks, newest first.  No scores.
+ *
+ * Tokens at or beyond seq_len are not part of any block.  An empty sequence
+ * gets an empty list.
+ */
+typedef enum { ART_LIST_IMPORTANCE = 0, ART_LIST_STREAMING = 1 } art_list_policy;
+typedef enum { ART_SCORE_KEY_NORM = 0, ART_SCORE_QUERY_BOUND = 1 } art_score_kind;
+
+typedef struct {
+    int32_t policy;        /* art_list_policy */
+    int32_t score_kind;    /* an art_score_kind; importance lists only */
+    int32_t budget;        /* importance: blocks kept; streaming: recent blocks kept (>= 0) */
+    int32_t sink_blocks;   /* leading blocks always kept (>= 0) */
+    int32_t keep_last;     /* importance: 1 keeps the last (newest) block */
+} art_list_opts;
+
+/*
+ * Workspace bytes art_build_block_list needs for the block scores when it
+ * does not get a `block_scores` array: batch * num_kv_heads * max_blocks
+ * doubles.  max_blocks = ceil(max_pages_per_seq * page_size / block_size)
+ * must be at most 8192.  Shape fields used: batch, num_q_heads,
+ * num_kv_heads, head_dim (128), block_size, page_size (a power of two),
+ * num_pages, max_pages_per_seq, max_blocks_per_list (the row stride of the
+ * output, which must hold the longest list the options allow), list_per_head
+ * (must be 1) and the K strides (multiples of 8 elements).  Returns 0 and
+ * sets *status on invalid input.
+ */
+size_t art_block_list_workspace_bytes(const art_decode_shape* shape, const art_list_opts* opts,
+                                      int32_t* status);
+
+/*
+ * Build the lists on `stream` (asynchronous).
+ *   q            bf16 [batch][num_q_heads][head_dim] (ART_SCORE_QUERY_BOUND only;
+ *                may be NULL otherwise).
+ *   k_cache, page_table, seq_lens  as for art_decode_attention.  k_cache and
+ *                page_table may be NULL for streaming lists.
+ *   block_list   int32 [batch][num_kv_heads][max_blocks_per_list], out.  Entries
+ *                past a row's length are left as they were.
+ *   block_list_len int32 [batch][num_kv_heads], out.
+ *   block_scores NULL, or double [batch][num_kv_heads][max_blocks], out (the
+ *                importance scores; entries of blocks past a sequence's end are
+ *                left as they were).  When NULL, the workspace holds them.
+ *   workspace    device memory of art_block_list_workspace_bytes() bytes, or
+ *                none when block_scores is given or the list is streaming.
+ * The outputs feed art_decode_attention directly (list_per_head = 1).
+ */
+art_status art_build_block_list(const art_decode_shape* shape, const art_list_opts* opts,
+                                const void* q, const void* k_cache, const int32_t* page_table,
+                                const int32_t* seq_lens, int32_t* block_list,
+                                int32_t* block_list_len, double* block_scores,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

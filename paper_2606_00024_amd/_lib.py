@@ -23,7 +23,12 @@ OUT_BF16 = 1
 # every symbol include/art.h declares
 EXPORTS = ("art_abi_version", "art_status_str", "art_decode_workspace_bytes",
            "art_workspace_init", "art_decode_attention", "art_validate_inputs",
-           "art_workspace_status")
+           "art_workspace_status", "art_block_list_workspace_bytes", "art_build_block_list")
+
+LIST_IMPORTANCE = 0
+LIST_STREAMING = 1
+SCORE_KEY_NORM = 0
+SCORE_QUERY_BOUND = 1
 
 
 class DecodeShape(ctypes.Structure):
@@ -36,7 +41,7 @@ class DecodeShape(ctypes.Structure):
 
 
 # ART_ABI_VERSION of include/art.h that these structure layouts follow
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 
 class DecodeOpts(ctypes.Structure):
@@ -44,6 +49,11 @@ class DecodeOpts(ctypes.Structure):
                 ("phi", ctypes.c_float), ("patience", ctypes.c_int32),
                 ("dense_order", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
                 ("chunk_blocks", ctypes.c_int32), ("probe_stride", ctypes.c_int32)]
+
+
+class ListOpts(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "policy", "score_kind", "budget", "sink_blocks", "keep_last")]
 
 
 class ArtError(RuntimeError):
@@ -86,6 +96,13 @@ def load() -> ctypes.CDLL:
             ctypes.POINTER(ctypes.c_int64), i32p]
         lib.art_workspace_status.restype = ctypes.c_int
         lib.art_workspace_status.argtypes = [vp, ctypes.c_size_t, vp, i32p]
+        lib.art_block_list_workspace_bytes.restype = ctypes.c_size_t
+        lib.art_block_list_workspace_bytes.argtypes = [ctypes.POINTER(DecodeShape),
+                                                       ctypes.POINTER(ListOpts), i32p]
+        lib.art_build_block_list.restype = ctypes.c_int
+        lib.art_build_block_list.argtypes = [
+            ctypes.POINTER(DecodeShape), ctypes.POINTER(ListOpts), vp, vp, vp, vp, vp, vp, vp,
+            vp, ctypes.c_size_t, vp]
         got = int(lib.art_abi_version())
         if got != ABI_VERSION:
             raise RuntimeError(f"{LIB_PATH} has ABI version {got}, this binding needs "
@@ -140,3 +157,21 @@ def workspace_status(ptr: int, nbytes: int, stream: int) -> int:
     if st != OK:
         raise ArtError(st, "art_workspace_status")
     return int(dev.value)
+
+
+def block_list_workspace_bytes(shape: DecodeShape, opts: ListOpts) -> int:
+    st = ctypes.c_int32(0)
+    n = load().art_block_list_workspace_bytes(ctypes.byref(shape), ctypes.byref(opts),
+                                              ctypes.byref(st))
+    if st.value != OK:
+        raise ArtError(st.value, "art_block_list_workspace_bytes")
+    return int(n)
+
+
+def build_block_list(shape, opts, q, k, page_table, seq_lens, block_list, block_list_len,
+                     block_scores, workspace, workspace_bytes, stream) -> int:
+    """Raw call; pointers are ints (0 for NULL).  Returns the status."""
+    return int(load().art_build_block_list(
+        ctypes.byref(shape), ctypes.byref(opts), q or None, k or None, page_table or None,
+        seq_lens, block_list, block_list_len, block_scores or None, workspace or None,
+        workspace_bytes, stream or None))

@@ -173,3 +173,47 @@ def validate_inputs(q, k_cache, v_cache, page_table, seq_lens, *, block_size: in
 def workspace_status(ws: torch.Tensor) -> int:
     """ART_OK or ART_ERR_DEVICE_TIMEOUT for calls that used ``ws`` (syncs)."""
     return _lib.workspace_status(_ptr(ws), ws.numel(), torch.cuda.current_stream(ws.device).cuda_stream)
+
+
+def build_block_list(q: torch.Tensor, k_cache: torch.Tensor, page_table: torch.Tensor,
+                     seq_lens: torch.Tensor, *, block_size: int, budget: int,
+                     policy: int = _lib.LIST_IMPORTANCE, score_kind: int = _lib.SCORE_KEY_NORM,
+                     sink_blocks: int = 0, keep_last: bool = False,
+                     max_list: Optional[int] = None, return_scores: bool = False):
+    """Traversal lists for decode_attention (Sec. 3.4), built on the current
+    stream: importance-first (block scores, top-`budget` with forced sink /
+    last blocks, descending score) or streaming (sinks first, then the
+    `budget` most recent blocks).
+
+    q bf16 [B][Hq][D] (the shape source; read for the query bound only),
+    k_cache bf16 [P][Hkv][Ps][D], page_table int32 [B][max_pages], seq_lens
+    int32 [B].  Returns (block_list int32 [B][Hkv][max_list], block_list_len
+    int32 [B][Hkv]) and, with return_scores, the fp64 block scores
+    [B][Hkv][max_blocks].  Entries past a row's length are -1.
+    """
+    _require_cuda(q, "q", torch.bfloat16)
+    _require_cuda(k_cache, "k_cache", torch.bfloat16)
+    _require_cuda(page_table, "page_table", torch.int32)
+    _require_cuda(seq_lens, "seq_lens", torch.int32)
+    if not q.is_contiguous() or not page_table.is_contiguous() or not seq_lens.is_contiguous():
+        raise ValueError("q, page_table and seq_lens must be contiguous")
+    B, Hq, D = q.shape
+    P, Hkv, Ps, _ = k_cache.shape
+    max_blocks = (int(page_table.shape[1]) * Ps + block_size - 1) // block_size
+    if max_list is None:
+        max_list = max(1, max_blocks)
+    dev = q.device
+    bl = torch.full((B, Hkv, max_list), -1, dtype=torch.int32, device=dev)
+    bll = torch.zeros((B, Hkv), dtype=torch.int32, device=dev)
+    shape = make_shape(q, k_cache, k_cache, page_table, block_size=block_size, block_list=bl)
+    opts = _lib.ListOpts(policy=int(policy), score_kind=int(score_kind), budget=int(budget),
+                         sink_blocks=int(sink_blocks), keep_last=1 if keep_last else 0)
+    _lib.block_list_workspace_bytes(shape, opts)  # raises on invalid input
+    scores = torch.full((B, Hkv, max(1, max_blocks)), float("nan"), dtype=torch.float64,
+                        device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    st = _lib.build_block_list(shape, opts, _ptr(q), _ptr(k_cache), _ptr(page_table),
+                               _ptr(seq_lens), _ptr(bl), _ptr(bll), _ptr(scores), 0, 0, stream)
+    if st != _lib.OK:
+        raise ArtError(st, "art_build_block_list")
+    return (bl, bll, scores) if return_scores else (bl, bll)

@@ -1,0 +1,402 @@
+// Traversal lists for the decode call (Sec. 3.4): the importance-first list
+// of a policy that scores KV blocks, and the sink-preserving recency-first
+// list of a policy that keeps sink tokens plus a recent window.
+//
+// Two launches:
+//   1. block scores (importance lists only), one wavefront per KV block of a
+//      (sequence, KV head) group, written as doubles:
+//        key norm:    max over the block's tokens of sum_d k_d^2
+//        query bound: max over the group's query heads of
+//                     sum_d max(q_d * min_j k_jd, q_d * max_j k_jd)
+//      Every sum runs over d = 0, 1, ..., 127 in order in fp64, on exact
+//      products of bf16 values, so the scores do not depend on how the work
+//      is split: equal inputs give equal bits on any implementation that
+//      keeps that order.
+//   2. selection, one workgroup per group: a bitonic sort of (score, id)
+//      pairs in LDS, descending score and ascending id; the forced blocks
+//      (the first sink_blocks, and the last when asked) and the best others
+//      up to the budget are kept in sorted order.  Streaming lists need no
+//      scores: sinks in increasing order, then the most recent blocks.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "art.h"
+#include "art_internal.h"
+
+namespace art {
+namespace {
+
+constexpr int kListThreads = 1024;   // selection workgroup
+constexpr int kMaxListBlocks = 8192; // blocks per sequence the selection sorts in LDS
+
+struct ListParams {
+    int32_t batch, num_q_heads, num_kv_heads, block_size, page_shift, num_pages;
+    int32_t max_pages, max_blocks, max_list, sort_n;
+    int64_t ks_page, ks_head, ks_tok;
+    int32_t policy, score_kind, budget, sink_blocks, keep_last;
+    const uint16_t* q;
+    const uint16_t* k;
+    const int32_t* page_table;
+    const int32_t* seq_lens;
+    int32_t* list;
+    int32_t* list_len;
+    double* scores;   // [groups][max_blocks]
+};
+
+typedef unsigned int u32x4_l __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ double bf16_lo(uint32_t w) { return (double)__uint_as_float(w << 16); }
+__device__ __forceinline__ double bf16_hi(uint32_t w) { return (double)__uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ int seq_len_of(const ListParams& P, int b) {
+    const int64_t cap = (int64_t)P.max_pages << P.page_shift;
+    const int L = P.seq_lens[b];
+    return L < 0 ? 0 : (int)(L > cap ? cap : L);
+}
+
+__device__ __forceinline__ const uint16_t* key_row(const ListParams& P, int b, int kvh, int tok) {
+    int pg = P.page_table[(int64_t)b * P.max_pages + (tok >> P.page_shift)];
+    pg = pg < 0 ? 0 : (pg >= P.num_pages ? P.num_pages - 1 : pg);
+    return P.k + pg * P.ks_page + kvh * P.ks_head + (int64_t)(tok & ((1 << P.page_shift) - 1)) * P.ks_tok;
+}
+
+// wave-wide max of a double (exact)
+__device__ __forceinline__ double wave_max(double x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = fmax(x, __shfl_xor(x, o));
+    return x;
+}
+
+// One wavefront per block: lane j takes token j of each 64-token slice and
+// sums its 128 squares in order.
+__global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int groups = P.batch * P.num_kv_heads;
+    if (wid >= (int64_t)groups * P.max_blocks) return;
+    const int gidx = (int)(wid / P.max_blocks), blk = (int)(wid % P.max_blocks);
+    const int b = gidx / P.num_kv_heads, kvh = gidx % P.num_kv_heads;
+    const int L = seq_len_of(P, b);
+    const int j0 = blk * P.block_size;
+    if (j0 >= L) return;
+    const int j1 = min(j0 + P.block_size, L);
+    double best = -1.0;   // below any sum of squares
+    for (int t0 = j0; t0 < j1; t0 += 64) {
+        const int j = t0 + lane;
+        if (j < j1) {
+            const u32x4_l* row = reinterpret_cast<const u32x4_l*>(key_row(P, b, kvh, j));
+            double s = 0.0;
+            for (int c = 0; c < 16; ++c) {
+                const u32x4_l w = row[c];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const double x0 = bf16_lo(w[e]), x1 = bf16_hi(w[e]);
+                    s = s + x0 * x0;   // dimension 8c + 2e
+                    s = s + x1 * x1;   // dimension 8c + 2e + 1
+                }
+            }
+            best = fmax(best, s);
+        }
+    }
+    best = wave_max(best);
+    if (lane == 0) P.scores[(int64_t)gidx * P.max_blocks + blk] = best;
+}
+
+// One wavefront per block: lane l keeps the extremes of dimensions 2l and
+// 2l + 1 over the block's tokens (one coalesced 256-byte row per step), the
+// per-dimension terms of every query head go to LDS, and lane h sums head
+// h's 128 terms in order.
+template <int G>
+__global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams P) {
+    __shared__ double terms[4][G][128];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t wid = (int64_t)blockIdx.x * 4 + w;
+    const int groups = P.batch * P.num_kv_heads;
+    if (wid >= (int64_t)groups * P.max_blocks) return;
+    const int gidx = (int)(wid / P.max_blocks), blk = (int)(wid % P.max_blocks);
+    const int b = gidx / P.num_kv_heads, kvh = gidx % P.num_kv_heads;
+    const int L = seq_len_of(P, b);
+    const int j0 = blk * P.block_size;
+    if (j0 >= L) return;
+    const int j1 = min(j0 + P.block_size, L);
+    float lo0 = 0.f, lo1 = 0.f, hi0 = 0.f, hi1 = 0.f;
+    for (int j = j0; j < j1; ++j) {
+        const uint32_t v = reinterpret_cast<const uint32_t*>(key_row(P, b, kvh, j))[lane];
+        const float x0 = __uint_as_float(v << 16), x1 = __uint_as_float(v & 0xffff0000u);
+        if (j == j0) {
+            lo0 = hi0 = x0;
+            lo1 = hi1 = x1;
+        } else {
+            lo0 = fminf(lo0, x0); hi0 = fmaxf(hi0, x0);
+            lo1 = fminf(lo1, x1); hi1 = fmaxf(hi1, x1);
+        }
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        const uint32_t qw = reinterpret_cast<const uint32_t*>(
+            P.q + ((int64_t)b * P.num_q_heads + kvh * G + h) * kHeadDim)[lane];
+        const double q0 = bf16_lo(qw), q1 = bf16_hi(qw);
+        terms[w][h][2 * lane] = fmax(q0 * (double)lo0, q0 * (double)hi0);
+        terms[w][h][2 * lane + 1] = fmax(q1 * (double)lo1, q1 * (double)hi1);
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+    double s = -INFINITY;
+    if (lane < G) {
+        s = 0.0;
+        for (int d = 0; d < 128; ++d) s = s + terms[w][lane][d];
+    }
+    s = wave_max(s);
+    if (lane == 0) P.scores[(int64_t)gidx * P.max_blocks + blk] = s;
+}
+
+// a before b: larger score, then smaller id
+__device__ __forceinline__ bool before(double sa, int ia, double sb, int ib) {
+    return sa > sb || (sa == sb && ia < ib);
+}
+
+// exclusive prefix sum of one int per thread over the workgroup
+__device__ int block_exclusive_scan(int v, int* scratch, int& total) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) scratch[w] = incl;
+    __syncthreads();
+    if (w == 0) {
+        const int nw = kListThreads / 64;
+        int x = lane < nw ? scratch[lane] : 0;
+        int xi = x;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(xi, o);
+            if (lane >= o) xi += y;
+        }
+        if (lane < nw) scratch[lane] = xi - x;   // exclusive offset of wave `lane`
+        if (lane == nw - 1) scratch[nw] = xi;    // total
+    }
+    __syncthreads();
+    const int r = scratch[w] + incl - v;
+    total = scratch[kListThreads / 64];
+    __syncthreads();
+    return r;
+}
+
+__global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P) {
+    extern __shared__ __align__(16) unsigned char lds[];
+    const int gidx = blockIdx.x, tid = threadIdx.x;
+    const int b = gidx / P.num_kv_heads;
+    const int L = seq_len_of(P, b);
+    const int n = L > 0 ? (L + P.block_size - 1) / P.block_size : 0;
+    int32_t* out = P.list + (int64_t)gidx * P.max_list;
+    if (P.policy == ART_LIST_STREAMING) {
+        const int ns = min(P.sink_blocks, n);
+        const int nr = min(P.budget, n - ns);
+        for (int i = tid; i < ns + nr; i += kListThreads) out[i] = i < ns ? i : n - 1 - (i - ns);
+        if (tid == 0) P.list_len[gidx] = ns + nr;
+        return;
+    }
+    // importance: sort (score, id) pairs of blocks 0..n-1, padded to sort_n
+    const int N = P.sort_n;
+    double* key = reinterpret_cast<double*>(lds);
+    int* id = reinterpret_cast<int*>(lds + (size_t)N * sizeof(double));
+    int* scratch = id + N;
+    const double* sc = P.scores + (int64_t)gidx * P.max_blocks;
+    for (int i = tid; i < N; i += kListThreads) {
+        key[i] = i < n ? sc[i] : -INFINITY;
+        id[i] = i < n ? i : 0x7fffffff;
+    }
+    __syncthreads();
+    for (int size = 2; size <= N; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = tid; i < N; i += kListThreads) {
+                const int j = i ^ stride;
+                if (j > i) {
+                    const bool up = (i & size) == 0;   // this run sorts "before" first
+                    const bool swap = up ? before(key[j], id[j], key[i], id[i])
+                                         : before(key[i], id[i], key[j], id[j]);
+                    if (swap) {
+                        const double tk = key[i]; key[i] = key[j]; key[j] = tk;
+                        const int ti = id[i]; id[i] = id[j]; id[j] = ti;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // forced blocks and the budget for the others
+    const int ns = min(P.sink_blocks, n);
+    const int nf = ns + ((P.keep_last && n > 0 && n - 1 >= ns) ? 1 : 0);
+    const int others = max(0, P.budget - nf);
+    // each thread takes a run of consecutive sorted positions
+    const int per = (N + kListThreads - 1) / kListThreads;
+    const int p0 = tid * per;
+    int cnt_other = 0;
+    for (int p = p0; p < min(p0 + per, n); ++p) {
+        const int i = id[p];
+        const bool forced = i < ns || (P.keep_last && i == n - 1);
+        cnt_other += forced ? 0 : 1;
+    }
+    int tot;
+    int rank_other = block_exclusive_scan(cnt_other, scratch, tot);
+    int cnt_sel = 0;
+    {
+        int r = rank_other;
+        for (int p = p0; p < min(p0 + per, n); ++p) {
+            const int i = id[p];
+            const bool forced = i < ns || (P.keep_last && i == n - 1);
+            if (forced) ++cnt_sel;
+            else { if (r < others) ++cnt_sel; ++r; }
+        }
+    }
+    int total_sel;
+    int pos = block_exclusive_scan(cnt_sel, scratch, total_sel);
+    {
+        int r = rank_other;
+        for (int p = p0; p < min(p0 + per, n); ++p) {
+            const int i = id[p];
+            const bool forced = i < ns || (P.keep_last && i == n - 1);
+            bool take = forced;
+            if (!forced) { take = r < others; ++r; }
+            if (take) out[pos++] = i;
+        }
+    }
+    if (tid == 0) P.list_len[gidx] = total_sel;
+}
+
+int ilog2_exact(int v) {
+    int s = 0;
+    while ((1 << s) < v) ++s;
+    return (1 << s) == v ? s : -1;
+}
+
+art_status check_list(const art_decode_shape* s, const art_list_opts* o, int& max_blocks, int& sort_n) {
+    if (!s || !o) return ART_ERR_INVALID_ARG;
+    if (s->batch < 0 || s->num_kv_heads <= 0 || s->num_q_heads <= 0 ||
+        s->num_q_heads % s->num_kv_heads != 0 || s->block_size <= 0 || s->page_size <= 0 ||
+        s->num_pages <= 0 || s->max_pages_per_seq <= 0 || s->max_blocks_per_list <= 0 ||
+        s->list_per_head != 1 || s->k_stride_page < 0 || s->k_stride_head < 0 || s->k_stride_token < 0)
+        return ART_ERR_INVALID_ARG;
+    if ((o->policy != ART_LIST_IMPORTANCE && o->policy != ART_LIST_STREAMING) || o->budget < 0 ||
+        o->sink_blocks < 0 || (o->keep_last != 0 && o->keep_last != 1) ||
+        (o->policy == ART_LIST_IMPORTANCE && o->score_kind != ART_SCORE_KEY_NORM &&
+         o->score_kind != ART_SCORE_QUERY_BOUND))
+        return ART_ERR_INVALID_ARG;
+    const int g = s->num_q_heads / s->num_kv_heads;
+    if (s->head_dim != kHeadDim || ilog2_exact(s->page_size) < 0) return ART_ERR_UNSUPPORTED;
+    if (o->policy == ART_LIST_IMPORTANCE && o->score_kind == ART_SCORE_QUERY_BOUND &&
+        g != 1 && g != 2 && g != 4 && g != 8 && g != 16)
+        return ART_ERR_UNSUPPORTED;
+    const int64_t mb = ((int64_t)s->max_pages_per_seq * s->page_size + s->block_size - 1) / s->block_size;
+    if (mb > kMaxListBlocks) return ART_ERR_UNSUPPORTED;
+    max_blocks = (int)mb;
+    sort_n = 1;
+    while (sort_n < max_blocks) sort_n <<= 1;
+    // the longest list this call can write must fit a row
+    int64_t longest;
+    if (o->policy == ART_LIST_STREAMING) {
+        longest = std::min<int64_t>(mb, (int64_t)o->sink_blocks + o->budget);
+    } else {
+        const int64_t forced = std::min<int64_t>(mb, o->sink_blocks) + (o->keep_last ? 1 : 0);
+        longest = std::min<int64_t>(mb, std::max<int64_t>(o->budget, forced));
+    }
+    if (longest > s->max_blocks_per_list) return ART_ERR_INVALID_ARG;
+    return ART_OK;
+}
+
+}  // namespace
+}  // namespace art
+
+extern "C" {
+
+size_t art_block_list_workspace_bytes(const art_decode_shape* shape, const art_list_opts* opts,
+                                      int32_t* status) {
+    int mb = 0, sn = 0;
+    const art_status st = art::check_list(shape, opts, mb, sn);
+    if (status) *status = st;
+    if (st != ART_OK) return 0;
+    return (size_t)shape->batch * shape->num_kv_heads * mb * sizeof(double);
+}
+
+art_status art_build_block_list(const art_decode_shape* shape, const art_list_opts* opts,
+                                const void* q, const void* k_cache, const int32_t* page_table,
+                                const int32_t* seq_lens, int32_t* block_list,
+                                int32_t* block_list_len, double* block_scores, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+    using namespace art;
+    int mb = 0, sn = 0;
+    art_status st = check_list(shape, opts, mb, sn);
+    if (st != ART_OK) return st;
+    if (shape->batch == 0) return ART_OK;
+    const bool importance = opts->policy == ART_LIST_IMPORTANCE;
+    if (!seq_lens || !block_list || !block_list_len) return ART_ERR_INVALID_ARG;
+    if (importance && (!k_cache || !page_table)) return ART_ERR_INVALID_ARG;
+    if (importance && opts->score_kind == ART_SCORE_QUERY_BOUND && !q) return ART_ERR_INVALID_ARG;
+    if (importance && (((uintptr_t)k_cache | (uintptr_t)(q ? q : k_cache)) % 16 ||
+                       shape->k_stride_token % 8 || shape->k_stride_head % 8 || shape->k_stride_page % 8))
+        return ART_ERR_UNSUPPORTED;
+    const size_t need = (size_t)shape->batch * shape->num_kv_heads * mb * sizeof(double);
+    double* scores = block_scores;
+    if (importance && !scores) {
+        if (!workspace || workspace_bytes < need) return ART_ERR_WORKSPACE_TOO_SMALL;
+        if ((uintptr_t)workspace % 8) return ART_ERR_INVALID_ARG;
+        scores = static_cast<double*>(workspace);
+    }
+    ListParams P;
+    memset(&P, 0, sizeof P);
+    P.batch = shape->batch;
+    P.num_q_heads = shape->num_q_heads;
+    P.num_kv_heads = shape->num_kv_heads;
+    P.block_size = shape->block_size;
+    P.page_shift = ilog2_exact(shape->page_size);
+    P.num_pages = shape->num_pages;
+    P.max_pages = shape->max_pages_per_seq;
+    P.max_blocks = mb;
+    P.max_list = shape->max_blocks_per_list;
+    P.sort_n = sn;
+    P.ks_page = shape->k_stride_page;
+    P.ks_head = shape->k_stride_head;
+    P.ks_tok = shape->k_stride_token;
+    P.policy = opts->policy;
+    P.score_kind = opts->score_kind;
+    P.budget = opts->budget;
+    P.sink_blocks = opts->sink_blocks;
+    P.keep_last = opts->keep_last;
+    P.q = static_cast<const uint16_t*>(q);
+    P.k = static_cast<const uint16_t*>(k_cache);
+    P.page_table = page_table;
+    P.seq_lens = seq_lens;
+    P.list = block_list;
+    P.list_len = block_list_len;
+    P.scores = scores;
+    const int groups = shape->batch * shape->num_kv_heads;
+    if (importance) {
+        const int64_t waves = (int64_t)groups * mb;
+        const dim3 grid((unsigned)((waves + 3) / 4));
+        if (opts->score_kind == ART_SCORE_KEY_NORM) {
+            hipLaunchKernelGGL(score_key_norm_kernel, grid, dim3(256), 0, stream, P);
+        } else {
+            switch (shape->num_q_heads / shape->num_kv_heads) {
+                case 1: hipLaunchKernelGGL(score_query_bound_kernel<1>, grid, dim3(256), 0, stream, P); break;
+                case 2: hipLaunchKernelGGL(score_query_bound_kernel<2>, grid, dim3(256), 0, stream, P); break;
+                case 4: hipLaunchKernelGGL(score_query_bound_kernel<4>, grid, dim3(256), 0, stream, P); break;
+                case 8: hipLaunchKernelGGL(score_query_bound_kernel<8>, grid, dim3(256), 0, stream, P); break;
+                default: hipLaunchKernelGGL(score_query_bound_kernel<16>, grid, dim3(256), 0, stream, P); break;
+            }
+        }
+        if (hipGetLastError() != hipSuccess) return ART_ERR_HIP;
+    }
+    const size_t lds = importance ? (size_t)sn * (sizeof(double) + sizeof(int)) +
+                                        (kListThreads / 64 + 1) * sizeof(int)
+                                  : 0;
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)groups), dim3(kListThreads), lds, stream, P);
+    return hipGetLastError() == hipSuccess ? ART_OK : ART_ERR_HIP;
+}
+
+}  // extern "C"

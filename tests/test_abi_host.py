@@ -153,3 +153,62 @@ def test_empty_batch_is_a_no_op(lib):
 
 def test_graft_entry_builds(lib):
     import __graft_entry__  # noqa: F401  (import only: build() is exercised by the driver)
+
+
+def _lopts(**kw):
+    d = dict(policy=_lib.LIST_IMPORTANCE, score_kind=_lib.SCORE_KEY_NORM, budget=4, sink_blocks=1,
+             keep_last=1)
+    d.update(kw)
+    return _lib.ListOpts(**d)
+
+
+def _lws(shape, opts):
+    st = ctypes.c_int32(-1)
+    n = _lib.load().art_block_list_workspace_bytes(ctypes.byref(shape), ctypes.byref(opts),
+                                                   ctypes.byref(st))
+    return n, st.value
+
+
+def test_block_list_workspace_is_the_score_array(lib):
+    # 16 pages of 64 tokens, blocks of 64: 16 blocks per sequence
+    n, st = _lws(_shape(max_blocks_per_list=16), _lopts())
+    assert (n, st) == (2 * 2 * 16 * 8, _lib.OK)
+    n, st = _lws(_shape(max_blocks_per_list=16, block_size=128), _lopts(score_kind=_lib.SCORE_QUERY_BOUND))
+    assert (n, st) == (2 * 2 * 8 * 8, _lib.OK)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(budget=-1), _lib.ERR_INVALID_ARG),
+    (dict(policy=2), _lib.ERR_INVALID_ARG),
+    (dict(score_kind=3), _lib.ERR_INVALID_ARG),
+    (dict(keep_last=2), _lib.ERR_INVALID_ARG),
+    (dict(sink_blocks=-1), _lib.ERR_INVALID_ARG),
+    (dict(budget=17), _lib.OK),                       # capped by the 16 blocks a sequence has
+    (dict(policy=_lib.LIST_STREAMING, budget=3, sink_blocks=2), _lib.OK),
+])
+def test_block_list_option_errors(lib, kw, status):
+    assert _lws(_shape(max_blocks_per_list=16), _lopts(**kw))[1] == status
+
+
+def test_block_list_shape_errors(lib):
+    # the row must hold the longest list the options allow
+    assert _lws(_shape(max_blocks_per_list=3), _lopts(budget=4))[1] == _lib.ERR_INVALID_ARG
+    assert _lws(_shape(max_blocks_per_list=4), _lopts(budget=4))[1] == _lib.OK
+    assert _lws(_shape(max_blocks_per_list=4), _lopts(policy=_lib.LIST_STREAMING, budget=3,
+                                                      sink_blocks=2))[1] == _lib.ERR_INVALID_ARG
+    # per-sequence lists are not produced; more than 8192 blocks per sequence are not sorted
+    assert _lws(_shape(max_blocks_per_list=16, list_per_head=0), _lopts())[1] == _lib.ERR_INVALID_ARG
+    assert _lws(_shape(max_blocks_per_list=16, max_pages_per_seq=8193), _lopts())[1] == _lib.ERR_UNSUPPORTED
+    assert _lws(_shape(max_blocks_per_list=16, page_size=48), _lopts())[1] == _lib.ERR_UNSUPPORTED
+    assert _lws(_shape(max_blocks_per_list=16, num_q_heads=6),
+                _lopts(score_kind=_lib.SCORE_QUERY_BOUND))[1] == _lib.ERR_UNSUPPORTED
+
+
+def test_block_list_rejects_null_outputs_before_launch(lib):
+    shape = _shape(max_blocks_per_list=16)
+    st = lib.art_build_block_list(ctypes.byref(shape), ctypes.byref(_lopts()), None, None, None,
+                                  None, None, None, None, None, 0, None)
+    assert st == _lib.ERR_INVALID_ARG
+    empty = _shape(batch=0, max_blocks_per_list=16)
+    assert lib.art_build_block_list(ctypes.byref(empty), ctypes.byref(_lopts()), None, None, None,
+                                    None, None, None, None, None, 0, None) == _lib.OK
