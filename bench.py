@@ -81,6 +81,9 @@ def parse():
     ap.add_argument("--phi", type=float, default=None)
     ap.add_argument("--patience", type=int, default=None)
     ap.add_argument("--chunk-blocks", type=int, default=0)
+    ap.add_argument("--list-producer", action="store_true",
+                    help="measure the device-side traversal-list producer (block scores and "
+                         "selection) on the workload's shape instead of the decode step")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (the reference kernel for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -200,6 +203,59 @@ def cpu_baseline(wl, eligible_tokens, tau, phi, patience, budget_s):
                       f"groups, same thresholds) in {elapsed:.1f}s, {threads} OpenMP threads"}
 
 
+def list_producer_leg(args):
+    """Importance lists (25 % of the blocks, first and last forced) for the
+    workload's shape: kernel time per call and the achieved HBM rate on the
+    key bytes the scores read (every token of every group: 256 bytes)."""
+    import torch
+    from paper_2606_00024_amd import _lib, api, workloads as W
+    spec = W.WORKLOADS[args.workload]
+    print(f"[bench] generating {args.workload}", file=sys.stderr, flush=True)
+    wl = W.make_workload(spec, device="cuda:0")
+    s = spec
+    B, Hkv = s.batch, s.num_kv_heads
+    lens = wl.seq_lens.cpu().tolist()
+    max_blocks = (int(wl.page_table.shape[1]) * s.page_size + s.block_size - 1) // s.block_size
+    budget = max(1, max_blocks // 4)
+    bl = torch.full((B, Hkv, max_blocks), -1, dtype=torch.int32, device="cuda:0")
+    bll = torch.zeros((B, Hkv), dtype=torch.int32, device="cuda:0")
+    scores = torch.empty((B, Hkv, max_blocks), dtype=torch.float64, device="cuda:0")
+    shape = api.make_shape(wl.q, wl.k_cache, wl.k_cache, wl.page_table, block_size=s.block_size,
+                           block_list=bl)
+    stream = torch.cuda.current_stream().cuda_stream
+    key_bytes = sum(lens) * Hkv * s.head_dim * 2
+    out = {"metric": "traversal-list producer: key bytes read per second", "unit": "GB/s",
+           "config": {"workload": args.workload, "batch": B, "kv_heads": Hkv,
+                      "q_heads": s.num_q_heads, "seq_lens": sorted(set(lens)),
+                      "block_size": s.block_size, "max_blocks": max_blocks, "budget": budget,
+                      "sink_blocks": 1, "keep_last": 1},
+           "key_bytes": key_bytes, "steps": args.steps, "warmup": args.warmup}
+    for name, kind in (("key_norm", _lib.SCORE_KEY_NORM), ("query_bound", _lib.SCORE_QUERY_BOUND)):
+        opts = _lib.ListOpts(policy=_lib.LIST_IMPORTANCE, score_kind=kind, budget=budget,
+                             sink_blocks=1, keep_last=1)
+
+        def call():
+            st = _lib.build_block_list(shape, opts, int(wl.q.data_ptr()), int(wl.k_cache.data_ptr()),
+                                       int(wl.page_table.data_ptr()), int(wl.seq_lens.data_ptr()),
+                                       int(bl.data_ptr()), int(bll.data_ptr()),
+                                       int(scores.data_ptr()), 0, 0, stream)
+            if st != 0:
+                raise _lib.ArtError(st, "art_build_block_list")
+        for _ in range(args.warmup):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        out[name] = {"ms_per_call": ms, "key_gbps": key_bytes / (ms * 1e-3) / 1e9,
+                     "frac_of_8tbs": key_bytes / (ms * 1e-3) / 8e12}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -219,6 +275,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": 3}), flush=True)
+        return
+
+    if args.list_producer:
+        list_producer_leg(args)
         return
 
     spec = W.WORKLOADS[args.workload]

@@ -70,11 +70,34 @@ __device__ __forceinline__ double wave_max(double x) {
     return x;
 }
 
-// One wavefront per block: lane j takes token j of each 64-token slice and
-// sums its 128 squares in order.
+// A wavefront reads 64 tokens (one 16 KiB tile) of a block with coalesced
+// 16-byte loads: load i of lane l holds bytes 16*(l & 15) .. +15 of token
+// 4i + (l >> 4).  kTileU32x4 = 16 loads.
+constexpr int kTileLoads = 16;
+constexpr int kRowPitch = 272;   // bytes per token row in the LDS tile (256 + 16 of padding)
+
+__device__ __forceinline__ void load_tile(const ListParams& P, int b, int kvh, int t0, int j1, int lane,
+                                          u32x4_l (&v)[kTileLoads]) {
+#pragma unroll
+    for (int i = 0; i < kTileLoads; ++i) {
+        const int tok = t0 + 4 * i + (lane >> 4);
+        v[i] = tok < j1 ? reinterpret_cast<const u32x4_l*>(key_row(P, b, kvh, tok))[lane & 15]
+                        : u32x4_l{0u, 0u, 0u, 0u};
+    }
+}
+
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS accesses are done
+    __builtin_amdgcn_wave_barrier();
+}
+
+// One wavefront per block.  The tile goes through LDS, 32 tokens at a time,
+// so that lane j can sum the 128 squares of token j in dimension order.
 __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P) {
-    const int lane = threadIdx.x & 63;
-    const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    extern __shared__ __align__(16) unsigned char tiles[];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    unsigned char* tile = tiles + w * 32 * kRowPitch;
+    const int64_t wid = (int64_t)blockIdx.x * 4 + w;
     const int groups = P.batch * P.num_kv_heads;
     if (wid >= (int64_t)groups * P.max_blocks) return;
     const int gidx = (int)(wid / P.max_blocks), blk = (int)(wid % P.max_blocks);
@@ -85,30 +108,42 @@ __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P)
     const int j1 = min(j0 + P.block_size, L);
     double best = -1.0;   // below any sum of squares
     for (int t0 = j0; t0 < j1; t0 += 64) {
-        const int j = t0 + lane;
-        if (j < j1) {
-            const u32x4_l* row = reinterpret_cast<const u32x4_l*>(key_row(P, b, kvh, j));
-            double s = 0.0;
-            for (int c = 0; c < 16; ++c) {
-                const u32x4_l w = row[c];
+        u32x4_l v[kTileLoads];
+        load_tile(P, b, kvh, t0, j1, lane, v);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const double x0 = bf16_lo(w[e]), x1 = bf16_hi(w[e]);
-                    s = s + x0 * x0;   // dimension 8c + 2e
-                    s = s + x1 * x1;   // dimension 8c + 2e + 1
+        for (int half = 0; half < 2; ++half) {
+            // loads 8*half .. 8*half+7 hold tokens 32*half .. 32*half+31
+#pragma unroll
+            for (int i = 0; i < kTileLoads / 2; ++i)
+                *reinterpret_cast<u32x4_l*>(tile + (4 * i + (lane >> 4)) * kRowPitch + 16 * (lane & 15)) =
+                    v[8 * half + i];
+            wave_lds_fence();
+            if (lane < 32 && t0 + 32 * half + lane < j1) {
+                const unsigned char* row = tile + lane * kRowPitch;
+                double s = 0.0;
+#pragma unroll
+                for (int c = 0; c < 16; ++c) {
+                    const u32x4_l x = *reinterpret_cast<const u32x4_l*>(row + 16 * c);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const double x0 = bf16_lo(x[e]), x1 = bf16_hi(x[e]);
+                        s = s + x0 * x0;   // dimension 8c + 2e
+                        s = s + x1 * x1;   // dimension 8c + 2e + 1
+                    }
                 }
+                best = fmax(best, s);
             }
-            best = fmax(best, s);
+            wave_lds_fence();   // the rows are read before they are written again
         }
     }
     best = wave_max(best);
     if (lane == 0) P.scores[(int64_t)gidx * P.max_blocks + blk] = best;
 }
 
-// One wavefront per block: lane l keeps the extremes of dimensions 2l and
-// 2l + 1 over the block's tokens (one coalesced 256-byte row per step), the
-// per-dimension terms of every query head go to LDS, and lane h sums head
-// h's 128 terms in order.
+// One wavefront per block: lane l keeps the extremes of dimensions
+// 8*(l & 15) .. +7 over the tokens its loads cover; the four lane rows are
+// then combined, the per-dimension terms of every query head go to LDS, and
+// lane h sums head h's 128 terms in order.
 template <int G>
 __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams P) {
     __shared__ double terms[4][G][128];
@@ -122,28 +157,47 @@ __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams
     const int j0 = blk * P.block_size;
     if (j0 >= L) return;
     const int j1 = min(j0 + P.block_size, L);
-    float lo0 = 0.f, lo1 = 0.f, hi0 = 0.f, hi1 = 0.f;
-    for (int j = j0; j < j1; ++j) {
-        const uint32_t v = reinterpret_cast<const uint32_t*>(key_row(P, b, kvh, j))[lane];
-        const float x0 = __uint_as_float(v << 16), x1 = __uint_as_float(v & 0xffff0000u);
-        if (j == j0) {
-            lo0 = hi0 = x0;
-            lo1 = hi1 = x1;
-        } else {
-            lo0 = fminf(lo0, x0); hi0 = fmaxf(hi0, x0);
-            lo1 = fminf(lo1, x1); hi1 = fmaxf(hi1, x1);
+    float lo[8], hi[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }
+    for (int t0 = j0; t0 < j1; t0 += 64) {
+        u32x4_l v[kTileLoads];
+        load_tile(P, b, kvh, t0, j1, lane, v);
+#pragma unroll
+        for (int i = 0; i < kTileLoads; ++i) {
+            if (t0 + 4 * i + (lane >> 4) < j1) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float x0 = __uint_as_float(v[i][e] << 16), x1 = __uint_as_float(v[i][e] & 0xffff0000u);
+                    lo[2 * e] = fminf(lo[2 * e], x0); hi[2 * e] = fmaxf(hi[2 * e], x0);
+                    lo[2 * e + 1] = fminf(lo[2 * e + 1], x1); hi[2 * e + 1] = fmaxf(hi[2 * e + 1], x1);
+                }
+            }
         }
     }
+    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same dimensions
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        const uint32_t qw = reinterpret_cast<const uint32_t*>(
-            P.q + ((int64_t)b * P.num_q_heads + kvh * G + h) * kHeadDim)[lane];
-        const double q0 = bf16_lo(qw), q1 = bf16_hi(qw);
-        terms[w][h][2 * lane] = fmax(q0 * (double)lo0, q0 * (double)hi0);
-        terms[w][h][2 * lane + 1] = fmax(q1 * (double)lo1, q1 * (double)hi1);
+    for (int e = 0; e < 8; ++e) {
+        lo[e] = fminf(lo[e], __shfl_xor(lo[e], 16)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 16));
+        lo[e] = fminf(lo[e], __shfl_xor(lo[e], 32)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 32));
     }
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are done
-    __builtin_amdgcn_wave_barrier();
+    // lane row r writes the terms of heads r, r + 4, ...
+    const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+    for (int h0 = 0; h0 < G; h0 += 4) {
+        const int h = h0 + r;
+        if (h < G) {
+            const u32x4_l qw = reinterpret_cast<const u32x4_l*>(
+                P.q + ((int64_t)b * P.num_q_heads + kvh * G + h) * kHeadDim)[c];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const double q0 = bf16_lo(qw[e]), q1 = bf16_hi(qw[e]);
+                terms[w][h][8 * c + 2 * e] = fmax(q0 * (double)lo[2 * e], q0 * (double)hi[2 * e]);
+                terms[w][h][8 * c + 2 * e + 1] = fmax(q1 * (double)lo[2 * e + 1], q1 * (double)hi[2 * e + 1]);
+            }
+        }
+    }
+    wave_lds_fence();
     double s = -INFINITY;
     if (lane < G) {
         s = 0.0;
@@ -213,18 +267,18 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
         id[i] = i < n ? i : 0x7fffffff;
     }
     __syncthreads();
+    // bitonic sort; pair p of a stage compares positions i and i + stride
     for (int size = 2; size <= N; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = tid; i < N; i += kListThreads) {
-                const int j = i ^ stride;
-                if (j > i) {
-                    const bool up = (i & size) == 0;   // this run sorts "before" first
-                    const bool swap = up ? before(key[j], id[j], key[i], id[i])
-                                         : before(key[i], id[i], key[j], id[j]);
-                    if (swap) {
-                        const double tk = key[i]; key[i] = key[j]; key[j] = tk;
-                        const int ti = id[i]; id[i] = id[j]; id[j] = ti;
-                    }
+            for (int p = tid; p < N / 2; p += kListThreads) {
+                const int i = (p / stride) * 2 * stride + (p % stride), j = i + stride;
+                const bool up = (i & size) == 0;   // this run sorts "before" first
+                const double ki = key[i], kj = key[j];
+                const int ii = id[i], ij = id[j];
+                const bool swap = up ? before(kj, ij, ki, ii) : before(ki, ii, kj, ij);
+                if (swap) {
+                    key[i] = kj; key[j] = ki;
+                    id[i] = ij; id[j] = ii;
                 }
             }
             __syncthreads();
@@ -380,7 +434,7 @@ art_status art_build_block_list(const art_decode_shape* shape, const art_list_op
         const int64_t waves = (int64_t)groups * mb;
         const dim3 grid((unsigned)((waves + 3) / 4));
         if (opts->score_kind == ART_SCORE_KEY_NORM) {
-            hipLaunchKernelGGL(score_key_norm_kernel, grid, dim3(256), 0, stream, P);
+            hipLaunchKernelGGL(score_key_norm_kernel, grid, dim3(256), 4 * 32 * kRowPitch, stream, P);
         } else {
             switch (shape->num_q_heads / shape->num_kv_heads) {
                 case 1: hipLaunchKernelGGL(score_query_bound_kernel<1>, grid, dim3(256), 0, stream, P); break;
