@@ -40,7 +40,8 @@ class Shape(ctypes.Structure):
 class Opts(ctypes.Structure):
     _fields_ = [("scale", ctypes.c_double), ("tau", ctypes.c_double),
                 ("phi", ctypes.c_double), ("patience", ctypes.c_int32),
-                ("dense_order", ctypes.c_int32), ("probe_stride", ctypes.c_int32)]
+                ("dense_order", ctypes.c_int32), ("probe_stride", ctypes.c_int32),
+                ("scale_of_accumulator", ctypes.c_int32)]
 
 
 def build(force: bool = True) -> str:
@@ -146,7 +147,7 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
            dense_order: int = 0, block_list=None, block_list_len=None,
            list_per_head: bool = True, force_stop=None, group_mask=None,
            trace_steps: int = 0, num_threads: int = 0, probe_stride: int = 1,
-           _lib=None):
+           scale_of_accumulator: bool = False, _lib=None):
     """Run the oracle.
 
     q: bf16 [B][Hq][D]; k_cache/v_cache: bf16 [P][Hkv][Ps][D] (contiguous);
@@ -155,7 +156,8 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
     int32 [B][Hkv] or [B].  ``scale``, ``tau`` and ``phi`` are rounded to
     fp32 first, since the kernel receives fp32 values.  ``probe_stride`` s
     makes the stability test look at coordinates 0, s, 2s, ... of each head's
-    output only (1 = the whole output).
+    output only (1 = the whole output).  ``scale_of_accumulator`` takes
+    d_scale on the unnormalised accumulator l(t) o(t) instead of o(t).
 
     Returns dict(out fp64 [B][Hq][D], lse fp64 [B][Hq], stop int32 [B][Hkv],
     trace fp64 [B][Hkv][trace_steps][g][2] or None).
@@ -183,7 +185,8 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
                v_stride_page=Hkv * Ps * D, v_stride_head=Ps * D, v_stride_token=D)
     op = Opts(scale=float(np.float32(scale)), tau=float(np.float32(tau)),
               phi=float(np.float32(phi)), patience=int(patience),
-              dense_order=int(dense_order), probe_stride=int(probe_stride))
+              dense_order=int(dense_order), probe_stride=int(probe_stride),
+              scale_of_accumulator=1 if scale_of_accumulator else 0)
     g = Hq // Hkv
     out = np.zeros((B, Hq, D), dtype=np.float64)
     lse = np.full((B, Hq), np.nan, dtype=np.float64)
@@ -206,7 +209,7 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
 
 def decode_workload(wl, *, tau=None, phi=None, patience=None, dense_order=None,
                     force_stop=None, group_mask=None, trace_steps=0, num_threads=0,
-                    probe_stride=1, _lib=None):
+                    probe_stride=1, scale_of_accumulator=False, _lib=None):
     """Oracle on a ``paper_2606_00024_amd.workloads.Workload`` (host copies)."""
     s = wl.spec
     return decode(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens,
@@ -218,4 +221,5 @@ def decode_workload(wl, *, tau=None, phi=None, patience=None, dense_order=None,
                   block_list=wl.block_list, block_list_len=wl.block_list_len,
                   force_stop=force_stop, group_mask=group_mask,
                   trace_steps=trace_steps, num_threads=num_threads,
-                  probe_stride=probe_stride, _lib=_lib)
+                  probe_stride=probe_stride, scale_of_accumulator=scale_of_accumulator,
+                  _lib=_lib)

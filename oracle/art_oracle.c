@@ -33,7 +33,12 @@
  *      head dimension, in place of Sec. 3.2's subsample taken from the
  *      accumulator's register layout (m = 32 there, i.e. s = 4 at D = 128).
  *   R2 o(t) is the normalised running output (Appendix A), not the
- *      unnormalised accumulator.
+ *      unnormalised accumulator.  With scale_of_accumulator set, d_scale is
+ *      taken instead on X(t) = l(t) o(t), the accumulator Algorithm 1 carries
+ *      before its final normalisation: l(t) = sum over the consumed tokens of
+ *      exp(s - m(t)), m(t) the running maximum score, each X in its own
+ *      step's reference (no rescaling of X(t-1)).  d_direction is the same
+ *      either way (l > 0 does not change a cosine).
  *   R3 grouped-query attention: one decision per (sequence, KV head); a step is
  *      stable only if it is stable for every query head of the group.
  *   R4 step 1 compares against o(0) = 0: cos is 0/0, the comparison is false,
@@ -116,8 +121,10 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
     double* u    = (double*)malloc(sizeof(double) * g * D);
     double* s    = (double*)malloc(sizeof(double) * g * Bk);
     double* logA = (double*)malloc(sizeof(double) * g);
+    double* mrun = (double*)malloc(sizeof(double) * g);             /* running max score */
     for (int i = 0; i < g; ++i) {
         logA[i] = -INFINITY;                                         /* A(0) = 0 */
+        mrun[i] = -INFINITY;
         const uint16_t* qh = q + ((int64_t)b * S->num_q_heads + kvh * g + i) * D;
         for (int d = 0; d < D; ++d) qd[i * D + d] = bf16_to_double(qh[d]);
     }
@@ -164,6 +171,13 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
             const double logl = mb + log(ssum);
             const double logA_new = log_add_exp(logA[i], logl);
             const double keep = exp(logA[i] - logA_new);   /* A(t-1) / A(t) */
+            /* R2 variant: accumulator weights l(t-1), l(t) in their own references */
+            const double m_new = mb > mrun[i] ? mb : mrun[i];
+            const double l_old = (logA[i] == -INFINITY) ? 0.0 : exp(logA[i] - mrun[i]);
+            const double l_new = exp(logA_new - m_new);
+            const double xs_new = O->scale_of_accumulator ? l_new : 1.0;
+            const double xs_old = O->scale_of_accumulator ? l_old : 1.0;
+            mrun[i] = m_new;
             const double w = exp(logl - logA_new);         /* l(t) / A(t)   */
             logA[i] = logA_new;
             /* o(t) = (A(t-1) o(t-1) + l(t) u(t)) / A(t) */
@@ -173,7 +187,7 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
             double ds2 = 0.0, dot = 0.0, n_new = 0.0, n_old = 0.0;
             for (int d = 0; d < D; d += ps) {
                 const double x = onew[i * D + d], x0 = o[i * D + d];
-                const double diff = x - x0;
+                const double diff = xs_new * x - xs_old * x0;
                 ds2 += diff * diff;
                 dot += x * x0;
                 n_new += x * x;
@@ -226,7 +240,7 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
                 }
         }
     }
-    free(list); free(qd); free(o); free(onew); free(u); free(s); free(logA);
+    free(list); free(qd); free(o); free(onew); free(u); free(s); free(logA); free(mrun);
     return rc;
 }
 

@@ -53,6 +53,10 @@ typedef struct {
     int32_t probe_stride; /* probe x = P o (Sec. 3.2, Appendix A): 1 = the whole
                              output (P = I); s > 1 (s divides head_dim) = the
                              coordinates 0, s, 2s, ... of o (m = head_dim / s) */
+    int32_t scale_of_accumulator; /* 1: d_scale on the unnormalised accumulator
+                             l(t) o(t), l(t) = sum of exp(s - running max), as
+                             Algorithm 1 keeps it before its final normalisation
+                             (R2 variant); 0: on o(t) */
 } artref_opts;
 
 enum {

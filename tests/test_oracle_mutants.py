@@ -110,6 +110,43 @@ def _battery(lib) -> list[str]:
     return sorted(set(fails))
 
 
+ACCUMULATOR_MUTANTS = {
+    "accumulator_old_in_new_reference": ("const double xs_old = O->scale_of_accumulator ? l_old : 1.0;",
+                                         "const double xs_old = O->scale_of_accumulator ? l_new : 1.0;"),
+    "accumulator_without_max_shift": ("const double l_new = exp(logA_new - m_new);",
+                                      "const double l_new = exp(logA_new);"),
+}
+
+
+def _accumulator_battery(lib) -> list[str]:
+    import test_oracle_accumulator as A
+    fails = []
+    for fn, args in ((A.test_bruteforce_stop_and_trace, (A.CASES[0], (5.0, 1e-3, 2))),
+                     (A.test_equal_scores_count_tokens, (10,))):
+        saved = oracle._lib
+        try:
+            oracle._lib = lib
+            fn(*args)
+        except AssertionError:
+            fails.append(fn.__name__)
+        finally:
+            oracle._lib = saved
+    return fails
+
+
+@pytest.mark.parametrize("name", sorted(ACCUMULATOR_MUTANTS))
+def test_planted_accumulator_mistake_is_caught(name, tmp_path):
+    old, new = ACCUMULATOR_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.load_library(oracle.build_variant(src.replace(old, new), str(tmp_path / f"{name}.so")))
+    assert _accumulator_battery(lib), f"planted mistake '{name}' passed every accumulator pin"
+
+
+def test_accumulator_battery_passes_on_the_real_oracle():
+    assert _accumulator_battery(oracle._load()) == []
+
+
 PROBE_MUTANTS = {
     "probe_stride_ignored": ("for (int d = 0; d < D; d += ps) {", "for (int d = 0; d < D; d += 1) {"),
     "probe_offset_shifted": ("for (int d = 0; d < D; d += ps) {",
