@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 3
+#define ART_ABI_VERSION 4
 
 typedef enum {
     ART_OK = 0,
@@ -111,6 +111,13 @@ typedef struct {
  * head_dim / s values spread over the head dimension, a fixed stand-in for
  * the subsample Sec. 3.2 takes from the accumulator's register layout; the
  * paper's m = 32 is s = 4).  The output and lse are always the full ones.
+ *
+ * scale_of_accumulator = 1 takes d_scale on the unnormalised accumulator
+ * X(t) = l(t) o(t) instead of o(t).  Here l(t) is the sum of exp(s - m(t))
+ * over the consumed tokens, with m(t) the running maximum score.  X(t) is
+ * what Algorithm 1 carries before its final normalisation, each step in its
+ * own reference.  The other reading of Algorithm 1; d_direction is the same
+ * under both.
  */
 typedef struct {
     float softmax_scale;           /* usually 1/sqrt(head_dim) (Eq. 1) */
@@ -121,6 +128,7 @@ typedef struct {
     int32_t out_dtype;             /* art_out_dtype */
     int32_t chunk_blocks;          /* 0 = automatic */
     int32_t probe_stride;          /* 0 or 1 = whole output; s > 1 = every s-th coordinate */
+    int32_t scale_of_accumulator;  /* 0: d_scale on o(t); 1: on the accumulator l(t) o(t) */
 } art_decode_opts;
 
 /* Version of this ABI (ART_ABI_VERSION). */

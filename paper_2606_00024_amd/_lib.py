@@ -41,14 +41,15 @@ class DecodeShape(ctypes.Structure):
 
 
 # ART_ABI_VERSION of include/art.h that these structure layouts follow
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class DecodeOpts(ctypes.Structure):
     _fields_ = [("softmax_scale", ctypes.c_float), ("tau", ctypes.c_float),
                 ("phi", ctypes.c_float), ("patience", ctypes.c_int32),
                 ("dense_order", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
-                ("chunk_blocks", ctypes.c_int32), ("probe_stride", ctypes.c_int32)]
+                ("chunk_blocks", ctypes.c_int32), ("probe_stride", ctypes.c_int32),
+                ("scale_of_accumulator", ctypes.c_int32)]
 
 
 class ListOpts(ctypes.Structure):

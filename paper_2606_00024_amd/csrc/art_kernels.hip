@@ -975,35 +975,48 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
       for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(s.o[kk][e] * pw[e], s.o[kk][e], n0);
       n_prev[kk] = row_sum(n0);
     }
+    const bool on_acc = P.scale_of_accumulator != 0;
     for (int i0 = 0; i0 < nb; i0 += NB) {
-      float pdd[NB][HPL], pod[NB][HPL], pn1[NB][HPL];
+      float pdd[NB][HPL], pod[NB][HPL], pn1[NB][HPL], pdx[NB][HPL];
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
 #pragma unroll
-        for (int kk = 0; kk < HPL; ++kk) pdd[u][kk] = pod[u][kk] = pn1[u][kk] = 0.f;
+        for (int kk = 0; kk < HPL; ++kk) pdd[u][kk] = pod[u][kk] = pn1[u][kk] = pdx[u][kk] = 0.f;
         const int i = i0 + u;
         if (i < nb) {
           State<G> blkst;
           read_tile<G>(blocks + i * REC, blkst, lane);
-          float old_o[HPL][8];
+          float old_o[HPL][8], old_L[HPL];
 #pragma unroll
-          for (int kk = 0; kk < HPL; ++kk)
+          for (int kk = 0; kk < HPL; ++kk) {
+            old_L[kk] = s.L[kk];
 #pragma unroll
             for (int e = 0; e < 8; ++e) old_o[kk][e] = s.o[kk][e];
+          }
           float d[HPL][8];
           merge<G, true>(s, blkst, d);
 #pragma unroll
           for (int kk = 0; kk < HPL; ++kk) {
-            float dd = 0.f, od = 0.f, n1 = 0.f;
+            float dd = 0.f, od = 0.f, n1 = 0.f, dx2 = 0.f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
               dd = __builtin_fmaf(d[kk][e] * pw[e], d[kk][e], dd);
               od = __builtin_fmaf(old_o[kk][e] * pw[e], d[kk][e], od);
               n1 = __builtin_fmaf(s.o[kk][e] * pw[e], s.o[kk][e], n1);
             }
+            if (on_acc) {
+              // change of the unnormalised accumulator L o, each side in its
+              // own max reference (L is the mass relative to the running max)
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float dx = __fsub_rn(__fmul_rn(s.L[kk], s.o[kk][e]), __fmul_rn(old_L[kk], old_o[kk][e]));
+                dx2 = __builtin_fmaf(dx * pw[e], dx, dx2);
+              }
+            }
             pdd[u][kk] = dd;
             pod[u][kk] = od;
             pn1[u][kk] = n1;
+            pdx[u][kk] = dx2;
           }
           write_state<G>(blocks + i * REC, s, lane);   // o(t) after block i, for the output
         }
@@ -1016,6 +1029,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
           pdd[u][kk] = row_sum(pdd[u][kk]);
           pod[u][kk] = row_sum(pod[u][kk]);
           pn1[u][kk] = row_sum(pn1[u][kk]);
+          if (on_acc) pdx[u][kk] = row_sum(pdx[u][kk]);
         }
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
@@ -1026,8 +1040,9 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
         for (int kk = 0; kk < HPL; ++kk) {
           const float n0 = n_prev[kk], dd = pdd[u][kk], od = pod[u][kk], n1 = pn1[u][kk];
           n_prev[kk] = n1;
-          // Eq. (2) on the probe: d_scale = |P d|; d_direction = 1 - cos(P o_new, P o_old)
-          const float d_scale = fast_sqrt(dd);
+          // Eq. (2) on the probe: d_scale = |P d| (or the change of P L o);
+          // d_direction = 1 - cos(P o_new, P o_old)
+          const float d_scale = fast_sqrt(on_acc ? pdx[u][kk] : dd);
           const float nn = __fmul_rn(fast_sqrt(n1), fast_sqrt(n0));
           const float dot = __fadd_rn(n0, od);
           float d_dir;

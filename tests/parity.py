@@ -47,20 +47,23 @@ def _rel_l2(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     return np.where(den > 0, num / np.maximum(den, 1e-300), num)
 
 
-def near_tie(trace_g: np.ndarray, upto: int, tau: float, phi: float) -> bool:
-    """trace_g [steps][g][2] of one group."""
+def near_tie(trace_g: np.ndarray, upto: int, tau: float, phi: float, tau_rel=None) -> bool:
+    """trace_g [steps][g][2] of one group.  The d_scale band is TIE_BAND, or
+    tau_rel * tau when given (the accumulator reading, whose d_scale is a
+    difference of two accumulators and carries their fp32 error)."""
     t = trace_g[: max(0, upto)]
     if t.size == 0:
         return False
     ds, dr = t[..., 0], t[..., 1]
     tau32, phi32 = float(np.float32(tau)), float(np.float32(phi))
+    band = TIE_BAND if tau_rel is None else tau_rel * tau32
     with np.errstate(invalid="ignore"):
-        hit = (np.abs(ds - tau32) <= TIE_BAND) | (np.abs(dr - phi32) <= TIE_BAND)
+        hit = (np.abs(ds - tau32) <= band) | (np.abs(dr - phi32) <= TIE_BAND)
     return bool(np.nan_to_num(hit).any())
 
 
 def compare_group(rep: Report, tag, out_g, lse_g, stop_g, ref_out, ref_lse, ref_stop, trace_g,
-                  tau, phi, rerun):
+                  tau, phi, rerun, tau_rel=None):
     """One (b, kvh) group.  out_g/ref_out [g][D]; rerun(stop) -> (out, lse)
     of the oracle forced to stop at `stop`."""
     rep.groups += 1
@@ -68,7 +71,7 @@ def compare_group(rep: Report, tag, out_g, lse_g, stop_g, ref_out, ref_lse, ref_
         rep.stop_equal += 1
         o_ref, l_ref = ref_out, ref_lse
     else:
-        if trace_g is None or not near_tie(trace_g, max(stop_g, ref_stop), tau, phi):
+        if trace_g is None or not near_tie(trace_g, max(stop_g, ref_stop), tau, phi, tau_rel):
             rep.failures.append((tag, "stop", int(stop_g), int(ref_stop)))
             return
         rep.near_ties.append((tag, int(stop_g), int(ref_stop)))
@@ -88,7 +91,8 @@ def compare_group(rep: Report, tag, out_g, lse_g, stop_g, ref_out, ref_lse, ref_
 
 
 def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=None,
-                     num_threads=0, probe_stride=1) -> Report:
+                     num_threads=0, probe_stride=1, scale_of_accumulator=False,
+                     tau_rel=None) -> Report:
     """Whole workload (small sizes): oracle on every group."""
     rep = report or Report()
     s = wl.spec
@@ -99,7 +103,8 @@ def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=No
     do = s.dense_order if dense_order is None else dense_order
     ref = oracle.decode_workload(wl, tau=tau, phi=phi, patience=patience, dense_order=do,
                                  trace_steps=T, num_threads=num_threads,
-                                 probe_stride=probe_stride)
+                                 probe_stride=probe_stride,
+                                 scale_of_accumulator=scale_of_accumulator)
     for b in range(s.batch):
         for h in range(s.num_kv_heads):
             def rerun(st, b=b, h=h):
@@ -109,12 +114,14 @@ def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=No
                 m[b, h] = 1
                 r = oracle.decode_workload(wl, tau=tau, phi=phi, patience=patience,
                                            dense_order=do, force_stop=fs, group_mask=m,
-                                           probe_stride=probe_stride)
+                                           probe_stride=probe_stride,
+                                           scale_of_accumulator=scale_of_accumulator)
                 return r["out"][b, h * g:(h + 1) * g], r["lse"][b, h * g:(h + 1) * g]
             compare_group(rep, (b, h), out[b, h * g:(h + 1) * g].astype(np.float64),
                           lse[b, h * g:(h + 1) * g].astype(np.float64), int(stop[b, h]),
                           ref["out"][b, h * g:(h + 1) * g], ref["lse"][b, h * g:(h + 1) * g],
-                          int(ref["stop"][b, h]), ref["trace"][b, h], tau, phi, rerun)
+                          int(ref["stop"][b, h]), ref["trace"][b, h], tau, phi, rerun,
+                          tau_rel)
     return rep
 
 

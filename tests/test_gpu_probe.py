@@ -176,3 +176,44 @@ def test_agreement_matches_the_oracle():
     a_ref = classify(host[4]["stop"], host[1]["stop"], T)
     assert (a_dev.agree, a_dev.fp, a_dev.fn, a_dev.both_stop_differ) == \
         (a_ref.agree, a_ref.fp, a_ref.fn, a_ref.both_stop_differ)
+
+
+# ---- the accumulator reading of d_scale (scale_of_accumulator) ----------------
+# d_scale is then a difference of two unnormalised accumulators l(t) o(t),
+# l(t) up to the number of tokens consumed; each carries the fp32 error of
+# its merges (about 1e-6 relative after a thousand), so the near-tie band for
+# d_scale is relative: 1e-3 of tau.
+ACC_TAU_REL = 1e-3
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"s{c[0]}" for c in CASES])
+def test_accumulator_reading_matrix(case):
+    seed, B, hkv, g, L, bk, ps, lists = case
+    wl = small_workload(seed, batch=B, kv_heads=hkv, group=g, seq_len=L, block_size=bk,
+                        page_size=ps, needles=2)
+    if lists:
+        wl.block_list, wl.block_list_len = random_lists(wl, seed, fraction=0.6)
+    _to_dev(wl)
+    for tau, phi, p in [(1.0, 1e-3, 2), (10.0, 1e-2, 3), (50.0, 1e-4, 5), (0.0, 1e-3, 2)]:
+        for stride in (1, 4):
+            _say(f"  gpu call: accumulator s{seed} stride={stride} tau={tau} phi={phi} p={p}")
+            gpu = api.decode_workload(wl, tau=tau, phi=phi, patience=p, probe_stride=stride,
+                                      scale_of_accumulator=True)
+            torch.cuda.synchronize()
+            rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, probe_stride=stride,
+                                   scale_of_accumulator=True, tau_rel=ACC_TAU_REL)
+            _say("  ", rep)
+            assert rep.ok(), str(rep)
+
+
+def test_accumulator_reading_closed_form():
+    """Equal scores, every value row e_0: X(t) = l(t) e_0 grows by 64 per
+    full block, so tau = 64.1 stops at p + 1 and tau = 63.9 never (the
+    normalised reading sees no change at all)."""
+    T, p = 8, 3
+    vec = np.zeros(D)
+    vec[0] = 1.0
+    q, k, v, pt, sl = uniform_key_case([vec] * T)
+    kw = dict(softmax_scale=0.088, phi=1e-6, patience=p, scale_of_accumulator=True)
+    assert int(_run_raw(q, k, v, pt, sl, tau=64.1, **kw)[2][0, 0]) == p + 1
+    assert int(_run_raw(q, k, v, pt, sl, tau=63.9, **kw)[2][0, 0]) == T
