@@ -41,7 +41,7 @@ class Opts(ctypes.Structure):
     _fields_ = [("scale", ctypes.c_double), ("tau", ctypes.c_double),
                 ("phi", ctypes.c_double), ("patience", ctypes.c_int32),
                 ("dense_order", ctypes.c_int32), ("probe_stride", ctypes.c_int32),
-                ("scale_of_accumulator", ctypes.c_int32)]
+                ("scale_of_accumulator", ctypes.c_int32), ("per_head_stop", ctypes.c_int32)]
 
 
 def build(force: bool = True) -> str:
@@ -147,7 +147,7 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
            dense_order: int = 0, block_list=None, block_list_len=None,
            list_per_head: bool = True, force_stop=None, group_mask=None,
            trace_steps: int = 0, num_threads: int = 0, probe_stride: int = 1,
-           scale_of_accumulator: bool = False, _lib=None):
+           scale_of_accumulator: bool = False, per_head_stop: bool = False, _lib=None):
     """Run the oracle.
 
     q: bf16 [B][Hq][D]; k_cache/v_cache: bf16 [P][Hkv][Ps][D] (contiguous);
@@ -158,6 +158,8 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
     makes the stability test look at coordinates 0, s, 2s, ... of each head's
     output only (1 = the whole output).  ``scale_of_accumulator`` takes
     d_scale on the unnormalised accumulator l(t) o(t) instead of o(t).
+    ``per_head_stop`` gives every query head its own counter and stop
+    (force_stop is then [B][Hq]); the result then has ``head_stop`` [B][Hq].
 
     Returns dict(out fp64 [B][Hq][D], lse fp64 [B][Hq], stop int32 [B][Hkv],
     trace fp64 [B][Hkv][trace_steps][g][2] or None).
@@ -186,11 +188,13 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
     op = Opts(scale=float(np.float32(scale)), tau=float(np.float32(tau)),
               phi=float(np.float32(phi)), patience=int(patience),
               dense_order=int(dense_order), probe_stride=int(probe_stride),
-              scale_of_accumulator=1 if scale_of_accumulator else 0)
+              scale_of_accumulator=1 if scale_of_accumulator else 0,
+              per_head_stop=1 if per_head_stop else 0)
     g = Hq // Hkv
     out = np.zeros((B, Hq, D), dtype=np.float64)
     lse = np.full((B, Hq), np.nan, dtype=np.float64)
     stop = np.full((B, Hkv), -1, dtype=np.int32)
+    head_stop = np.full((B, Hq), -1, dtype=np.int32)
     trace = np.full((B, Hkv, trace_steps, g, 2), np.nan) if trace_steps > 0 else None
     err = ctypes.c_int32(-1)
     rc = lib.artref_decode(
@@ -200,16 +204,18 @@ def decode(q, k_cache, v_cache, page_table, seq_lens, *, block_size: int,
         _ptr(bl, ctypes.c_int32), _ptr(bll, ctypes.c_int32), _ptr(fs, ctypes.c_int32),
         _ptr(gm, ctypes.c_uint8),
         _ptr(out, ctypes.c_double), _ptr(lse, ctypes.c_double), _ptr(stop, ctypes.c_int32),
+        _ptr(head_stop, ctypes.c_int32),
         _ptr(trace, ctypes.c_double), ctypes.c_int32(trace_steps),
         ctypes.c_int32(num_threads), ctypes.byref(err))
     if rc != OK:
         raise OracleError(rc, err.value)
-    return {"out": out, "lse": lse, "stop": stop, "trace": trace}
+    return {"out": out, "lse": lse, "stop": stop, "head_stop": head_stop, "trace": trace}
 
 
 def decode_workload(wl, *, tau=None, phi=None, patience=None, dense_order=None,
                     force_stop=None, group_mask=None, trace_steps=0, num_threads=0,
-                    probe_stride=1, scale_of_accumulator=False, _lib=None):
+                    probe_stride=1, scale_of_accumulator=False, per_head_stop=False,
+                    _lib=None):
     """Oracle on a ``paper_2606_00024_amd.workloads.Workload`` (host copies)."""
     s = wl.spec
     return decode(wl.q, wl.k_cache, wl.v_cache, wl.page_table, wl.seq_lens,
@@ -222,4 +228,4 @@ def decode_workload(wl, *, tau=None, phi=None, patience=None, dense_order=None,
                   force_stop=force_stop, group_mask=group_mask,
                   trace_steps=trace_steps, num_threads=num_threads,
                   probe_stride=probe_stride, scale_of_accumulator=scale_of_accumulator,
-                  _lib=_lib)
+                  per_head_stop=per_head_stop, _lib=_lib)

@@ -40,7 +40,10 @@
  *      step's reference (no rescaling of X(t-1)).  d_direction is the same
  *      either way (l > 0 does not change a cosine).
  *   R3 grouped-query attention: one decision per (sequence, KV head); a step is
- *      stable only if it is stable for every query head of the group.
+ *      stable only if it is stable for every query head of the group.  With
+ *      per_head_stop set, each query head instead runs its own counter and
+ *      stops on its own (its output and lse are those of its stop); the group
+ *      reads blocks until its last head has stopped.
  *   R4 step 1 compares against o(0) = 0: cos is 0/0, the comparison is false,
  *      so step 1 is never stable.  Generally, a zero-norm vector makes the step
  *      unstable.
@@ -81,7 +84,8 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
                      const int32_t* page_table, const int32_t* seq_lens,
                      const int32_t* block_list, const int32_t* block_list_len,
                      const int32_t* force_stop, double* out, double* lse,
-                     int32_t* stop_block, double* trace, int32_t trace_steps) {
+                     int32_t* stop_block, int32_t* head_stop, double* trace,
+                     int32_t trace_steps) {
     const int g = S->num_q_heads / S->num_kv_heads;
     const int D = S->head_dim;
     const int Bk = S->block_size;
@@ -128,9 +132,14 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
         const uint16_t* qh = q + ((int64_t)b * S->num_q_heads + kvh * g + i) * D;
         for (int d = 0; d < D; ++d) qd[i * D + d] = bf16_to_double(qh[d]);
     }
-    int fstop = force_stop ? force_stop[gi] : 0;
+    const int per_head = O->per_head_stop;
+    int fstop = (force_stop && !per_head) ? force_stop[gi] : 0;
     int c = 0;      /* patience counter, Eq. (3) */
     int tstar = T;  /* no break: all T blocks consumed */
+    /* R3 variant: a counter and a stop per query head (0 = still reading) */
+    int* ch = (int*)calloc(g, sizeof(int));
+    int* hstop = (int*)calloc(g, sizeof(int));
+    int running = g;
 
     for (int t = 1; t <= T && !rc; ++t) {
         const int blk = list[t - 1];
@@ -201,6 +210,19 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
             /* Sec. 3.2 (R3: every head of the group must be stable) */
             const int stable = (d_scale < O->tau) && (d_dir < O->phi);
             if (!stable) all_stable = 0;
+            if (per_head && !hstop[i]) {
+                /* Eq. (3) and the break of Algorithm 1 for this head alone */
+                ch[i] = stable ? ch[i] + 1 : 0;
+                const int fh = force_stop ? force_stop[(int64_t)b * S->num_q_heads + kvh * g + i] : 0;
+                if ((fh >= 1) ? (t >= fh) : (ch[i] >= O->patience)) {
+                    hstop[i] = t;
+                    --running;
+                    const int h = kvh * g + i;
+                    double* oh = out + ((int64_t)b * S->num_q_heads + h) * D;
+                    for (int d = 0; d < D; ++d) oh[d] = keep * o[i * D + d] + w * u[i * D + d];
+                    lse[(int64_t)b * S->num_q_heads + h] = logA[i];
+                }
+            }
             if (trace && t <= trace_steps) {
                 double* tr = trace + (((int64_t)gi * trace_steps + (t - 1)) * g + i) * 2;
                 tr[0] = d_scale;
@@ -208,6 +230,10 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
             }
         }
         memcpy(o, onew, sizeof(double) * g * D);
+        if (per_head) {
+            if (running == 0) { tstar = t; break; }
+            continue;
+        }
         c = all_stable ? c + 1 : 0;                    /* Eq. (3) */
         if (fstop >= 1) {
             if (t >= fstop) { tstar = t; break; }
@@ -219,9 +245,14 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
     if (!rc) {
         for (int i = 0; i < g; ++i) {
             const int h = kvh * g + i;
+            if (per_head && hstop[i]) {       /* written at the head's own stop */
+                if (head_stop) head_stop[(int64_t)b * S->num_q_heads + h] = hstop[i];
+                continue;
+            }
             double* oh = out + ((int64_t)b * S->num_q_heads + h) * D;
             for (int d = 0; d < D; ++d) oh[d] = (T > 0) ? o[i * D + d] : 0.0;
             lse[(int64_t)b * S->num_q_heads + h] = (T > 0) ? logA[i] : -INFINITY;
+            if (head_stop) head_stop[(int64_t)b * S->num_q_heads + h] = (T > 0) ? tstar : 0;
         }
         stop_block[gi] = (T > 0) ? tstar : 0;
         if (trace) {
@@ -241,6 +272,7 @@ static int run_group(const artref_shape* S, const artref_opts* O, int b, int kvh
         }
     }
     free(list); free(qd); free(o); free(onew); free(u); free(s); free(logA); free(mrun);
+    free(ch); free(hstop);
     return rc;
 }
 
@@ -257,7 +289,7 @@ int artref_decode(const artref_shape* S, const artref_opts* O,
                   const int32_t* page_table, const int32_t* seq_lens,
                   const int32_t* block_list, const int32_t* block_list_len,
                   const int32_t* force_stop, const uint8_t* group_mask,
-                  double* out, double* lse, int32_t* stop_block,
+                  double* out, double* lse, int32_t* stop_block, int32_t* head_stop,
                   double* trace, int32_t trace_steps,
                   int32_t num_threads, int32_t* err_group) {
     if (err_group) *err_group = -1;
@@ -284,7 +316,7 @@ int artref_decode(const artref_shape* S, const artref_opts* O,
         const int b = gi / S->num_kv_heads, kvh = gi % S->num_kv_heads;
         int rc = run_group(S, O, b, kvh, q, k_cache, v_cache, page_table, seq_lens,
                            block_list, block_list_len, force_stop, out, lse, stop_block,
-                           trace, trace_steps);
+                           head_stop, trace, trace_steps);
         if (rc) {
 #ifdef _OPENMP
 #pragma omp critical

@@ -57,6 +57,9 @@ typedef struct {
                              l(t) o(t), l(t) = sum of exp(s - running max), as
                              Algorithm 1 keeps it before its final normalisation
                              (R2 variant); 0: on o(t) */
+    int32_t per_head_stop; /* 1: every query head has its own patience counter and
+                             stop (R3 variant); the group reads blocks until all its
+                             heads have stopped; 0: one stop per group */
 } artref_opts;
 
 enum {
@@ -73,7 +76,9 @@ enum {
  * group_mask: NULL, or [batch][num_kv_heads]; groups with 0 are skipped
  *   (their outputs are left untouched).
  * out [batch][num_q_heads][head_dim], lse [batch][num_q_heads] (fp64),
- * stop_block [batch][num_kv_heads].
+ * stop_block [batch][num_kv_heads] (blocks the group consumed).
+ * head_stop: NULL, or [batch][num_q_heads]: the stop of each query head (with
+ *   per_head_stop; otherwise its group's stop).
  * trace: NULL, or [batch][num_kv_heads][trace_steps][g][2] holding
  *   (d_scale, d_direction) for steps 1..min(T, trace_steps) (NaN elsewhere).
  * num_threads <= 0: OpenMP default.
@@ -84,7 +89,7 @@ int artref_decode(const artref_shape* shape, const artref_opts* opts,
                   const int32_t* page_table, const int32_t* seq_lens,
                   const int32_t* block_list, const int32_t* block_list_len,
                   const int32_t* force_stop, const uint8_t* group_mask,
-                  double* out, double* lse, int32_t* stop_block,
+                  double* out, double* lse, int32_t* stop_block, int32_t* head_stop,
                   double* trace, int32_t trace_steps,
                   int32_t num_threads, int32_t* err_group);
 

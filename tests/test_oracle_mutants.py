@@ -147,6 +147,47 @@ def test_accumulator_battery_passes_on_the_real_oracle():
     assert _accumulator_battery(oracle._load()) == []
 
 
+PER_HEAD_MUTANTS = {
+    "head_counter_not_reset": ("ch[i] = stable ? ch[i] + 1 : 0;", "ch[i] = stable ? ch[i] + 1 : ch[i];"),
+    "head_output_at_group_stop": ("if (per_head && hstop[i]) {       /* written at the head's own stop */",
+                                  "if (0 && per_head && hstop[i]) {"),
+}
+
+
+def _per_head_battery(lib) -> list[str]:
+    import test_oracle_per_head as H
+    fails = []
+    saved = oracle._lib
+    try:
+        oracle._lib = lib
+        for case in H.CASES:
+            for rule in H.RULES:
+                try:
+                    H.test_per_head_stops_and_outputs_match_brute_force(case, rule)
+                except AssertionError:
+                    fails.append(f"brute{case[0]}{rule}")
+        try:
+            H.test_interrupted_run_restarts_the_count()
+        except AssertionError:
+            fails.append("restart")
+    finally:
+        oracle._lib = saved
+    return fails
+
+
+@pytest.mark.parametrize("name", sorted(PER_HEAD_MUTANTS))
+def test_planted_per_head_mistake_is_caught(name, tmp_path):
+    old, new = PER_HEAD_MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    lib = oracle.load_library(oracle.build_variant(src.replace(old, new), str(tmp_path / f"{name}.so")))
+    assert _per_head_battery(lib), f"planted mistake '{name}' passed every per-head pin"
+
+
+def test_per_head_battery_passes_on_the_real_oracle():
+    assert _per_head_battery(oracle._load()) == []
+
+
 PROBE_MUTANTS = {
     "probe_stride_ignored": ("for (int d = 0; d < D; d += ps) {", "for (int d = 0; d < D; d += 1) {"),
     "probe_offset_shifted": ("for (int d = 0; d < D; d += ps) {",
