@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 4
+#define ART_ABI_VERSION 5
 
 typedef enum {
     ART_OK = 0,
@@ -129,6 +129,10 @@ typedef struct {
     int32_t chunk_blocks;          /* 0 = automatic */
     int32_t probe_stride;          /* 0 or 1 = whole output; s > 1 = every s-th coordinate */
     int32_t scale_of_accumulator;  /* 0: d_scale on o(t); 1: on the accumulator l(t) o(t) */
+    int32_t no_detector;           /* 1: no stability test at all (tau, phi, patience and
+                                      the probe options are ignored): full attention over
+                                      the traversal, stop_block = T; the baseline that
+                                      shows what the test itself costs */
 } art_decode_opts;
 
 /* Version of this ABI (ART_ABI_VERSION). */

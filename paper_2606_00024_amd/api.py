@@ -52,14 +52,16 @@ def make_shape(q, k_cache, v_cache, page_table, *, block_size: int, block_list=N
 
 def make_opts(*, softmax_scale: float, tau: float, phi: float, patience: int,
               dense_order: int = 0, out_dtype=torch.float32, chunk_blocks: int = 0,
-              probe_stride: int = 1, scale_of_accumulator: bool = False) -> DecodeOpts:
+              probe_stride: int = 1, scale_of_accumulator: bool = False,
+              no_detector: bool = False) -> DecodeOpts:
     od = _lib.OUT_BF16 if out_dtype == torch.bfloat16 else _lib.OUT_F32
     if out_dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_dtype must be float32 or bfloat16")
     return DecodeOpts(softmax_scale=float(softmax_scale), tau=float(tau), phi=float(phi),
                       patience=int(patience), dense_order=int(dense_order), out_dtype=od,
                       chunk_blocks=int(chunk_blocks), probe_stride=int(probe_stride),
-                      scale_of_accumulator=1 if scale_of_accumulator else 0)
+                      scale_of_accumulator=1 if scale_of_accumulator else 0,
+                      no_detector=1 if no_detector else 0)
 
 
 def workspace_bytes(shape: DecodeShape, opts: DecodeOpts) -> int:
@@ -93,7 +95,7 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                      block_list_len: Optional[torch.Tensor] = None,
                      list_per_head: bool = True, out_dtype=torch.float32,
                      chunk_blocks: int = 0, probe_stride: int = 1,
-                     scale_of_accumulator: bool = False,
+                     scale_of_accumulator: bool = False, no_detector: bool = False,
                      workspace: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      stop_block: Optional[torch.Tensor] = None):
@@ -105,7 +107,8 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     ``probe_stride`` s > 1 makes the stability test look at every s-th
     coordinate of each head's output only (Sec. 3.2's subsampled probe).
     ``scale_of_accumulator`` takes d_scale on the unnormalised accumulator
-    l(t) o(t) instead of o(t).
+    l(t) o(t) instead of o(t).  ``no_detector`` runs without the stability
+    test at all (full attention over the traversal).
     """
     _require_cuda(q, "q", torch.bfloat16)
     _require_cuda(k_cache, "k_cache", torch.bfloat16)
@@ -129,7 +132,8 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                        block_list=block_list, list_per_head=list_per_head)
     opts = make_opts(softmax_scale=softmax_scale, tau=tau, phi=phi, patience=patience,
                      dense_order=dense_order, out_dtype=out_dtype, chunk_blocks=chunk_blocks,
-                     probe_stride=probe_stride, scale_of_accumulator=scale_of_accumulator)
+                     probe_stride=probe_stride, scale_of_accumulator=scale_of_accumulator,
+                     no_detector=no_detector)
     dev = q.device
     if out is None:
         out = torch.empty((B, Hq, D), dtype=out_dtype, device=dev)

@@ -64,7 +64,8 @@ art_status check_shape(const art_decode_shape* s, const art_decode_opts* o) {
         o->chunk_blocks > art::kMaxChunkBlocks || o->probe_stride < 0 ||
         (o->probe_stride & (o->probe_stride - 1)) != 0 ||
         (o->probe_stride > 1 && s->head_dim % o->probe_stride != 0) ||
-        (o->scale_of_accumulator != 0 && o->scale_of_accumulator != 1))
+        (o->scale_of_accumulator != 0 && o->scale_of_accumulator != 1) ||
+        (o->no_detector != 0 && o->no_detector != 1))
         return ART_ERR_INVALID_ARG;
     const int g = s->num_q_heads / s->num_kv_heads;
     if (s->head_dim != art::kHeadDim) return ART_ERR_UNSUPPORTED;
@@ -237,6 +238,7 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.patience = opts->patience;
     k.probe_stride = opts->probe_stride > 1 ? opts->probe_stride : 1;
     k.scale_of_accumulator = opts->scale_of_accumulator;
+    k.no_detector = opts->no_detector;
     k.dense_order = opts->dense_order;
     k.out_bf16 = opts->out_dtype == ART_OUT_BF16;
     k.tiles_per_block = plan.tiles_per_block;

@@ -71,6 +71,7 @@ struct KernelParams {
     int32_t patience, dense_order, out_bf16;
     int32_t probe_stride;    // the stability test sees coordinates 0, s, 2s, ... (1 = all)
     int32_t scale_of_accumulator;  // 1: d_scale on the unnormalised accumulator L o
+    int32_t no_detector;     // 1: no stability test at all (full attention over the traversal)
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
     int32_t work_chunks;     // chunk rows of the work list (<= max_chunks)

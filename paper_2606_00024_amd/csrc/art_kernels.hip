@@ -943,6 +943,13 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     State<G> inc = pre;
     merge<G, false>(inc, agg);
     publish_state<G>(rs, rec_inc, inc, lane);
+    if (P.no_detector) {
+      // no stability test (the detector-free baseline): later chunks need
+      // only the inclusive state, and the last chunk holds the output
+      publish(P, gidx, k, kInclusive, lane);
+      if (k == n_chunks - 1) write_outputs<G>(P, b, kvh, inc, T, lane);
+      return;
+    }
   }
   bool incl_pending = true;
   auto raise_inclusive = [&]() {

@@ -92,7 +92,8 @@ def test_shape_errors(lib, kw, status):
     dict(tau=float("nan")), dict(phi=float("nan")), dict(patience=0), dict(dense_order=2),
     dict(out_dtype=5), dict(chunk_blocks=-1), dict(chunk_blocks=17),
     dict(softmax_scale=float("inf")), dict(probe_stride=-1), dict(probe_stride=3),
-    dict(probe_stride=6), dict(probe_stride=256),
+    dict(probe_stride=6), dict(probe_stride=256), dict(scale_of_accumulator=2),
+    dict(no_detector=-1), dict(no_detector=2),
 ])
 def test_option_errors(lib, kw):
     n, st = _ws(_shape(), _opts(**kw))

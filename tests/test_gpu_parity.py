@@ -269,3 +269,19 @@ def test_full_size(name, nsample):
         assert rep.ok(), str(rep)
     del wl
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[f"s{c[0]}" for c in SMALL])
+def test_no_detector_is_full_attention(case):
+    """no_detector = 1 skips the stability test altogether: every block of the
+    traversal is read and the result is the oracle with termination off,
+    whatever tau, phi and patience say."""
+    wl = _small(case)
+    _say(f"  gpu call: no_detector {wl.spec.name}")
+    gpu = api.decode_workload(wl, tau=0.5, phi=0.5, patience=1, no_detector=True)
+    torch.cuda.synchronize()
+    T = np.asarray(wl.traversal_lengths())
+    assert np.array_equal(gpu[2].cpu().numpy(), T)
+    rep = compare_workload(wl, gpu, tau=0.0, phi=1e-4, patience=5)
+    _say("  ", rep)
+    assert rep.ok(), str(rep)
