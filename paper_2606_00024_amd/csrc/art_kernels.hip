@@ -596,12 +596,27 @@ __device__ __forceinline__ StabState stab_fold(StabState x, StabSummary y, int t
   return r;
 }
 
-// The stop announcement of a group is one word: epoch << 24 | chunk.
+// The stop announcement of a group is one word: epoch << 24 | chunk, where
+// the chunk holds the stop or lies after it.  Chunks after the announced one
+// are moot: loaders skip them and their resolvers give up.
 __device__ __forceinline__ bool stop_word_before(uint64_t v, uint64_t epoch, int me) {
   return (v >> kQueueBits) == epoch && (int)(v & ((1ull << kQueueBits) - 1ull)) < me;
 }
 __device__ __forceinline__ bool stop_announced_before(const KernelParams& P, int gidx, int me) {
   return stop_word_before(ld_relaxed(P.stop_word + gidx), P.epoch, me);
+}
+// Lowers the announcement to chunk k unless this call already announced a
+// chunk <= k (a word of an earlier call, whatever its bits, is replaced).
+// Several chunks of a group may announce; each compare-and-swap that fails
+// saw another announcement land, so the loop ends.  Lane 0 only.
+__device__ void announce_stop(const KernelParams& P, int gidx, int k) {
+  uint64_t* w = P.stop_word + gidx;
+  const uint64_t mine = (P.epoch << kQueueBits) | (uint64_t)k;
+  uint64_t cur = ld_relaxed(w);
+  for (uint32_t spin = 0; !stop_word_before(cur, P.epoch, k + 1) && spin < P.spin_limit; ++spin)
+    if (__hip_atomic_compare_exchange_strong(w, &cur, mine, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT))
+      break;
 }
 
 // Look-back over the flags of chunks me-1, me-2, ... of group gidx, 64 per
@@ -1088,6 +1103,9 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     sm.fis = fis;
   }
   publish_word(P, gidx, k, kStabSummary, pack_summary(sm), lane);
+  // A run of p stable blocks inside this chunk puts the stop here or earlier,
+  // whatever the chunks before hold: the later chunks are moot from now on.
+  if (sm.fis >= 0 && lane == 0) announce_stop(P, gidx, k);
   // A chunk whose first block is unstable and whose own run never reaches
   // the patience cannot hold the stop, whatever run it enters with: unless
   // it is the last chunk (which writes the untruncated result) it is done.
@@ -1098,9 +1116,8 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   if (!stab_entering(P, gidx, k, x, lane)) return;
   const bool stopped_before = x.stopped != 0;
   const StabState y = stab_fold(x, sm, t0, P.patience);
-  if (!stopped_before && y.stopped && lane == 0)  // the stop lies in this chunk: announce it at once
-    __hip_atomic_store(P.stop_word + gidx, (P.epoch << kQueueBits) | (uint64_t)k, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+  if (!stopped_before && y.stopped && sm.fis < 0 && lane == 0)  // the stop lies in this chunk
+    announce_stop(P, gidx, k);
   publish_word(P, gidx, k, kStabInclusive, pack_stab(y), lane);
   wave_lds_sync();  // saved per-block states were written by other lanes
   if (!stopped_before && y.stopped) {
