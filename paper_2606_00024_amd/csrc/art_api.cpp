@@ -124,11 +124,14 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
         C = o->chunk_blocks;
     } else {
         // up to 9 blocks per chunk, a multiple of the three loaders when the
-        // budget allows; smaller chunks when the whole problem would not
-        // give the 256 CUs enough work
+        // budget allows; 6, then 3, only when the whole problem has fewer
+        // than 64 chunks.  (Measured: halving the chunk whenever there were
+        // fewer chunks than 1024 cost 17-210 % on problems of 2 to 16
+        // groups; the per-chunk work of the resolver outweighs the wider
+        // spread.)
         C = c_max < 9 ? c_max : 9;
         if (C >= 3) C -= C % 3;
-        while (C > 1 && n_groups * ((t_cap + C - 1) / C) < 1024) C /= 2;
+        while (C > 3 && n_groups * ((t_cap + C - 1) / C) < 64) C -= 3;
         // the work list must fit a queue word
         while (C < c_max && n_groups * ((t_cap + C - 1) / C) + art::kQueueSlack >= (1 << art::kQueueBits)) C *= 2;
     }
