@@ -40,6 +40,15 @@ uint64_t next_epoch() {
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+constexpr int kLeadChunks = 4;  // leading short chunks per traversal
+constexpr int kLeadBlocks = 3;  // blocks in each of them
+
+// Chunks of a traversal of T blocks (the kernel's chunks_for).
+int64_t chunks_for(int64_t T, int C, int lead_chunks, int lead_blocks) {
+    const int64_t lead_T = (int64_t)lead_chunks * lead_blocks;
+    return T <= lead_T ? (T + lead_blocks - 1) / lead_blocks : lead_chunks + (T - lead_T + C - 1) / C;
+}
+
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
 int ilog2(int64_t x) {
@@ -137,7 +146,17 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     }
     if (C > c_max) C = c_max;
     if (C < 1) C = 1;
-    const int64_t max_chunks = (t_cap + C - 1) / C;
+    // Leading chunks of kLeadBlocks blocks: the first decisions of every
+    // group come sooner, so that groups that stop early claim less past
+    // their stop (only with the default chunk size).
+    int lead_chunks = 0, lead_blocks = C;
+    if (o->chunk_blocks == 0 && C > kLeadBlocks) {
+        lead_chunks = kLeadChunks;
+        lead_blocks = kLeadBlocks;
+    }
+    p->lead_chunks = lead_chunks;
+    p->lead_blocks = lead_blocks;
+    const int64_t max_chunks = chunks_for(t_cap, C, lead_chunks, lead_blocks);
     if (n_groups * max_chunks + art::kQueueSlack >= (1 << art::kQueueBits)) return ART_ERR_UNSUPPORTED;
 
     p->group = g;
@@ -247,6 +266,8 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.tiles_per_block = plan.tiles_per_block;
     k.chunk_blocks = plan.chunk_blocks;
     k.max_chunks = plan.max_chunks;
+    k.lead_chunks = plan.lead_chunks;
+    k.lead_blocks = plan.lead_blocks;
     k.t_cap = plan.t_cap;
     k.n_slots = plan.slots;
     {
@@ -256,7 +277,7 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
                                    : (cap_tokens + shape->block_size - 1) / shape->block_size;
         if (t_eff > plan.t_cap) t_eff = plan.t_cap;
         if (t_eff < 1) t_eff = 1;
-        k.work_chunks = (int32_t)((t_eff + plan.chunk_blocks - 1) / plan.chunk_blocks);
+        k.work_chunks = (int32_t)chunks_for(t_eff, plan.chunk_blocks, plan.lead_chunks, plan.lead_blocks);
     }
     k.record_floats = plan.record_floats;
     k.chunk_recs_lds = plan.chunk_blocks;

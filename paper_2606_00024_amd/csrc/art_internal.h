@@ -49,6 +49,8 @@ struct Plan {
     int32_t group;           // query heads per KV head (g)
     int32_t tiles_per_block; // block_size / kTile
     int32_t chunk_blocks;    // blocks per chunk (C)
+    int32_t lead_chunks;     // leading chunks of a traversal that hold lead_blocks blocks
+    int32_t lead_blocks;
     int32_t max_chunks;      // chunks per group the grid provides
     int32_t n_groups;        // batch * num_kv_heads
     int32_t t_cap;           // traversal length bound per group
@@ -74,6 +76,7 @@ struct KernelParams {
     int32_t no_detector;     // 1: no stability test at all (full attention over the traversal)
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
+    int32_t lead_chunks, lead_blocks;  // the first lead_chunks chunks hold lead_blocks blocks
     int32_t work_chunks;     // chunk rows of the work list (<= max_chunks)
     int32_t chunk_recs_lds;  // block records per LDS chunk buffer
     int32_t loader_partials; // per-loader partial aggregates kept in LDS (3 or 0)

@@ -551,6 +551,18 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
 }
 
 // ---- phase 2 helpers ----------------------------------------------------------
+// Chunk geometry: the first lead_chunks chunks of a traversal hold
+// lead_blocks blocks each, every later one chunk_blocks.
+__device__ __forceinline__ int chunk_start(const KernelParams& P, int k) {
+  return k < P.lead_chunks ? k * P.lead_blocks
+                           : P.lead_chunks * P.lead_blocks + (k - P.lead_chunks) * P.chunk_blocks;
+}
+__device__ __forceinline__ int chunks_for(const KernelParams& P, int T) {
+  const int lead_T = P.lead_chunks * P.lead_blocks;
+  return T <= lead_T ? (T + P.lead_blocks - 1) / P.lead_blocks
+                     : P.lead_chunks + (T - lead_T + P.chunk_blocks - 1) / P.chunk_blocks;
+}
+
 struct StabSummary {   // one chunk's own blocks (entering run taken as 0)
   int32_t lead;        // leading stable blocks
   int32_t trail;       // trailing stable blocks
@@ -662,7 +674,6 @@ __device__ int lookback_scan(const KernelParams& P, int gidx, int me, uint32_t n
 // stop before `me` has been announced or the spin limit is reached.
 __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState& x, int lane) {
   const uint64_t* flags = P.flags + (int64_t)gidx * P.max_chunks;
-  const int C = P.chunk_blocks;
   int hi = me - 1, j = -1;
   uint32_t it = 0;
   while (hi >= 0) {
@@ -681,7 +692,7 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
         if (first < 64) x = unpack_stab(__builtin_amdgcn_readlane(pl, first));
         const int top = first < 64 ? first : hi + 1;
         for (int u = top - 1; u >= 0; --u)
-          x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), (hi - u) * C, P.patience);
+          x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), chunk_start(P, hi - u), P.patience);
         return true;
       }
       if (first < 64) {
@@ -706,7 +717,7 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
     const int n = min(64, me - i0);
     const uint32_t pl = lane < n ? flag_payload(ld_relaxed(flags + i0 + lane)) : 0u;
     for (int u = 0; u < n; ++u)
-      x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), (i0 + u) * C, P.patience);
+      x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), chunk_start(P, i0 + u), P.patience);
   }
   return true;
 }
@@ -789,7 +800,7 @@ __device__ __forceinline__ GroupInfo group_info_raw(const KernelParams& P, int g
   }
   if (g.nblk == 0) T = 0;
   g.T = min(T, P.t_cap);
-  g.n_chunks = (g.T + P.chunk_blocks - 1) / P.chunk_blocks;
+  g.n_chunks = chunks_for(P, g.T);
   return g;
 }
 
@@ -890,9 +901,8 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
                               float* blocks, const float* aggbuf, int nagg, int lane) {
   constexpr int REC = Cfg<G>::REC;
   const int b = gi.b, kvh = gi.kvh, T = gi.T, n_chunks = gi.n_chunks;
-  const int C = P.chunk_blocks;
-  const int t0 = k * C;
-  const int nb = min(C, T - t0);
+  const int t0 = chunk_start(P, k);
+  const int nb = min(chunk_start(P, k + 1), T) - t0;
   const __amdgpu_buffer_rsrc_t rs = record_rsrc(P, gidx);
   const int rec_agg = k * 2 * P.record_floats;          // float offsets in the group's area
   const int rec_inc = rec_agg + P.record_floats;
@@ -1264,8 +1274,8 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
     const int k = lds_ld(&s_meta[slot][kMetaChunk]);
     const GroupInfo gi = group_info_raw(P, gidx, lds_ld(&s_meta[slot][kMetaLen]),
                                         lds_ld(&s_meta[slot][kMetaListLen]));
-    const int t0 = k * P.chunk_blocks;
-    const int nb = min(P.chunk_blocks, gi.T - t0);
+    const int t0 = chunk_start(P, k);
+    const int nb = min(chunk_start(P, k + 1), gi.T) - t0;
     const int tpb = P.tiles_per_block;
     float* blocks = smem + slot * slot_floats;
     bool aborted = false;
