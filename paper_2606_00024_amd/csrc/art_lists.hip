@@ -57,11 +57,6 @@ __device__ __forceinline__ int seq_len_of(const ListParams& P, int b) {
     return L < 0 ? 0 : (int)(L > cap ? cap : L);
 }
 
-__device__ __forceinline__ const uint16_t* key_row(const ListParams& P, int b, int kvh, int tok) {
-    int pg = P.page_table[(int64_t)b * P.max_pages + (tok >> P.page_shift)];
-    pg = pg < 0 ? 0 : (pg >= P.num_pages ? P.num_pages - 1 : pg);
-    return P.k + pg * P.ks_page + kvh * P.ks_head + (int64_t)(tok & ((1 << P.page_shift) - 1)) * P.ks_tok;
-}
 
 // wave-wide max of a double (exact)
 __device__ __forceinline__ double wave_max(double x) {
@@ -72,17 +67,69 @@ __device__ __forceinline__ double wave_max(double x) {
 
 // A wavefront reads 64 tokens (one 16 KiB tile) of a block with coalesced
 // 16-byte loads: load i of lane l holds bytes 16*(l & 15) .. +15 of token
-// 4i + (l >> 4).  kTileU32x4 = 16 loads.
+// 4i + (l >> 4), which lies in 16-token piece i / 4 of the tile (a piece
+// never straddles a page: pages hold at least 16 tokens).
 constexpr int kTileLoads = 16;
 constexpr int kRowPitch = 272;   // bytes per token row in the LDS tile (256 + 16 of padding)
 
-__device__ __forceinline__ void load_tile(const ListParams& P, int b, int kvh, int t0, int j1, int lane,
+// The score kernels are persistent: wavefront w walks the blocks w, w + W,
+// ... of the flattened (group, block) range (W = wavefronts in the grid),
+// skipping blocks past their sequence's end, one 64-token tile at a time.
+// The loads of the next tile are issued before the current tile is
+// processed, and the page ids two tiles ahead before that, so that every
+// wavefront keeps one tile of keys in flight while it computes.
+struct TilePos {
+    int64_t item;   // flattened group * max_blocks + block; >= n_items when done
+    int gidx, b, kvh, blk, t0, j1;
+};
+
+// The first tile of the first block at or after `item` that holds tokens.
+__device__ __forceinline__ TilePos first_tile(const ListParams& P, int64_t item, int64_t stride,
+                                              int64_t n_items) {
+    TilePos t;
+    for (; item < n_items; item += stride) {
+        const int gidx = (int)(item / P.max_blocks), blk = (int)(item % P.max_blocks);
+        const int b = gidx / P.num_kv_heads;
+        const int L = seq_len_of(P, b);
+        const int j0 = blk * P.block_size;
+        if (j0 < L) {
+            t.gidx = gidx; t.b = b; t.kvh = gidx % P.num_kv_heads; t.blk = blk;
+            t.t0 = j0; t.j1 = min(j0 + P.block_size, L);
+            break;
+        }
+    }
+    t.item = item;
+    return t;
+}
+
+__device__ __forceinline__ TilePos next_tile(const ListParams& P, TilePos t, int64_t stride, int64_t n_items) {
+    if (t.t0 + 64 < t.j1) {
+        t.t0 += 64;
+        return t;
+    }
+    return first_tile(P, t.item + stride, stride, n_items);
+}
+
+// Page of 16-token piece n of the tile, in lane n (n < 4).
+__device__ __forceinline__ int tile_pages(const ListParams& P, const TilePos& t, int lane) {
+    int pg = 0;
+    if (t.item >= 0 && lane < 4) {
+        const int tok = min(t.t0 + 16 * lane, t.j1 - 1);
+        pg = P.page_table[(int64_t)t.b * P.max_pages + (tok >> P.page_shift)];
+        pg = pg < 0 ? 0 : (pg >= P.num_pages ? P.num_pages - 1 : pg);
+    }
+    return pg;
+}
+
+__device__ __forceinline__ void load_tile(const ListParams& P, const TilePos& t, int pages, int lane,
                                           u32x4_l (&v)[kTileLoads]) {
+    const int pmask = (1 << P.page_shift) - 1;
 #pragma unroll
     for (int i = 0; i < kTileLoads; ++i) {
-        const int tok = t0 + 4 * i + (lane >> 4);
-        v[i] = tok < j1 ? reinterpret_cast<const u32x4_l*>(key_row(P, b, kvh, tok))[lane & 15]
-                        : u32x4_l{0u, 0u, 0u, 0u};
+        const int tok = t.t0 + 4 * i + (lane >> 4);
+        const int pg = __builtin_amdgcn_readlane(pages, i >> 2);
+        const uint16_t* row = P.k + pg * P.ks_page + t.kvh * P.ks_head + (int64_t)(tok & pmask) * P.ks_tok;
+        v[i] = tok < t.j1 ? reinterpret_cast<const u32x4_l*>(row)[lane & 15] : u32x4_l{0u, 0u, 0u, 0u};
     }
 }
 
@@ -91,120 +138,155 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_wave_barrier();
 }
 
-// One wavefront per block.  The tile goes through LDS, 32 tokens at a time,
-// so that lane j can sum the 128 squares of token j in dimension order.
+// Walks this wavefront's tiles with the loads one tile ahead; `tile_fn(t, v)`
+// consumes a tile, `block_fn(t)` ends a block (after its last tile).
+template <class TileFn, class BlockFn>
+__device__ __forceinline__ void stream_tiles(const ListParams& P, TileFn tile_fn, BlockFn block_fn) {
+    const int lane = threadIdx.x & 63;
+    const int64_t stride = (int64_t)gridDim.x * 4;
+    const int64_t n_items = (int64_t)P.batch * P.num_kv_heads * P.max_blocks;
+    TilePos cur = first_tile(P, (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), stride, n_items);
+    if (cur.item >= n_items) return;
+    TilePos nxt = next_tile(P, cur, stride, n_items);
+    int pg_cur = tile_pages(P, cur, lane);
+    int pg_nxt = nxt.item < n_items ? tile_pages(P, nxt, lane) : 0;
+    u32x4_l v[kTileLoads];
+    load_tile(P, cur, pg_cur, lane, v);
+    for (;;) {
+        // two tiles ahead: its page ids; one tile ahead: its keys
+        const TilePos nn = nxt.item < n_items ? next_tile(P, nxt, stride, n_items) : nxt;
+        const int pg_nn = nn.item < n_items ? tile_pages(P, nn, lane) : 0;
+        u32x4_l w[kTileLoads];
+        if (nxt.item < n_items) load_tile(P, nxt, pg_nxt, lane, w);
+        tile_fn(cur, v);
+        if (nxt.item != cur.item) block_fn(cur);
+        if (nxt.item >= n_items) break;
+#pragma unroll
+        for (int i = 0; i < kTileLoads; ++i) v[i] = w[i];
+        cur = nxt;
+        nxt = nn;
+        pg_nxt = pg_nn;
+    }
+}
+
+// Lane j sums the 128 squares of token j in dimension order: the tile goes
+// through LDS, 32 tokens at a time.
 __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P) {
     extern __shared__ __align__(16) unsigned char tiles[];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     unsigned char* tile = tiles + w * 32 * kRowPitch;
-    const int64_t wid = (int64_t)blockIdx.x * 4 + w;
-    const int groups = P.batch * P.num_kv_heads;
-    if (wid >= (int64_t)groups * P.max_blocks) return;
-    const int gidx = (int)(wid / P.max_blocks), blk = (int)(wid % P.max_blocks);
-    const int b = gidx / P.num_kv_heads, kvh = gidx % P.num_kv_heads;
-    const int L = seq_len_of(P, b);
-    const int j0 = blk * P.block_size;
-    if (j0 >= L) return;
-    const int j1 = min(j0 + P.block_size, L);
     double best = -1.0;   // below any sum of squares
-    for (int t0 = j0; t0 < j1; t0 += 64) {
-        u32x4_l v[kTileLoads];
-        load_tile(P, b, kvh, t0, j1, lane, v);
+    stream_tiles(P,
+        [&](const TilePos& t, const u32x4_l (&v)[kTileLoads]) {
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            // loads 8*half .. 8*half+7 hold tokens 32*half .. 32*half+31
+            for (int half = 0; half < 2; ++half) {
+                // loads 8*half .. 8*half+7 hold tokens 32*half .. 32*half+31
 #pragma unroll
-            for (int i = 0; i < kTileLoads / 2; ++i)
-                *reinterpret_cast<u32x4_l*>(tile + (4 * i + (lane >> 4)) * kRowPitch + 16 * (lane & 15)) =
-                    v[8 * half + i];
-            wave_lds_fence();
-            if (lane < 32 && t0 + 32 * half + lane < j1) {
-                const unsigned char* row = tile + lane * kRowPitch;
-                double s = 0.0;
+                for (int i = 0; i < kTileLoads / 2; ++i)
+                    *reinterpret_cast<u32x4_l*>(tile + (4 * i + (lane >> 4)) * kRowPitch + 16 * (lane & 15)) =
+                        v[8 * half + i];
+                wave_lds_fence();
+                if (lane < 32 && t.t0 + 32 * half + lane < t.j1) {
+                    const unsigned char* row = tile + lane * kRowPitch;
+                    double s = 0.0;
 #pragma unroll
-                for (int c = 0; c < 16; ++c) {
-                    const u32x4_l x = *reinterpret_cast<const u32x4_l*>(row + 16 * c);
+                    for (int c = 0; c < 16; ++c) {
+                        const u32x4_l x = *reinterpret_cast<const u32x4_l*>(row + 16 * c);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const double x0 = bf16_lo(x[e]), x1 = bf16_hi(x[e]);
-                        s = s + x0 * x0;   // dimension 8c + 2e
-                        s = s + x1 * x1;   // dimension 8c + 2e + 1
+                        for (int e = 0; e < 4; ++e) {
+                            const double x0 = bf16_lo(x[e]), x1 = bf16_hi(x[e]);
+                            s = s + x0 * x0;   // dimension 8c + 2e
+                            s = s + x1 * x1;   // dimension 8c + 2e + 1
+                        }
                     }
+                    best = fmax(best, s);
                 }
-                best = fmax(best, s);
+                wave_lds_fence();   // the rows are read before they are written again
             }
-            wave_lds_fence();   // the rows are read before they are written again
-        }
-    }
-    best = wave_max(best);
-    if (lane == 0) P.scores[(int64_t)gidx * P.max_blocks + blk] = best;
+        },
+        [&](const TilePos& t) {
+            const double m = wave_max(best);
+            if (lane == 0) P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = m;
+            best = -1.0;
+        });
 }
 
-// One wavefront per block: lane l keeps the extremes of dimensions
-// 8*(l & 15) .. +7 over the tokens its loads cover; the four lane rows are
-// then combined, the per-dimension terms of every query head go to LDS, and
-// lane h sums head h's 128 terms in order.
+// Lane l keeps the extremes of dimensions 8*(l & 15) .. +7 over the tokens
+// its loads cover; at the end of a block the four lane rows are combined,
+// the per-dimension terms of every query head go to LDS, and lane h sums
+// head h's 128 terms in order.
 template <int G>
 __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams P) {
     __shared__ double terms[4][G][128];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int64_t wid = (int64_t)blockIdx.x * 4 + w;
-    const int groups = P.batch * P.num_kv_heads;
-    if (wid >= (int64_t)groups * P.max_blocks) return;
-    const int gidx = (int)(wid / P.max_blocks), blk = (int)(wid % P.max_blocks);
-    const int b = gidx / P.num_kv_heads, kvh = gidx % P.num_kv_heads;
-    const int L = seq_len_of(P, b);
-    const int j0 = blk * P.block_size;
-    if (j0 >= L) return;
-    const int j1 = min(j0 + P.block_size, L);
     float lo[8], hi[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }
-    for (int t0 = j0; t0 < j1; t0 += 64) {
-        u32x4_l v[kTileLoads];
-        load_tile(P, b, kvh, t0, j1, lane, v);
+    stream_tiles(P,
+        [&](const TilePos& t, const u32x4_l (&v)[kTileLoads]) {
 #pragma unroll
-        for (int i = 0; i < kTileLoads; ++i) {
-            if (t0 + 4 * i + (lane >> 4) < j1) {
+            for (int i = 0; i < kTileLoads; ++i) {
+                if (t.t0 + 4 * i + (lane >> 4) < t.j1) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float x0 = __uint_as_float(v[i][e] << 16), x1 = __uint_as_float(v[i][e] & 0xffff0000u);
-                    lo[2 * e] = fminf(lo[2 * e], x0); hi[2 * e] = fmaxf(hi[2 * e], x0);
-                    lo[2 * e + 1] = fminf(lo[2 * e + 1], x1); hi[2 * e + 1] = fmaxf(hi[2 * e + 1], x1);
+                    for (int e = 0; e < 4; ++e) {
+                        const float x0 = __uint_as_float(v[i][e] << 16), x1 = __uint_as_float(v[i][e] & 0xffff0000u);
+                        lo[2 * e] = fminf(lo[2 * e], x0); hi[2 * e] = fmaxf(hi[2 * e], x0);
+                        lo[2 * e + 1] = fminf(lo[2 * e + 1], x1); hi[2 * e + 1] = fmaxf(hi[2 * e + 1], x1);
+                    }
                 }
             }
-        }
-    }
-    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same dimensions
+        },
+        [&](const TilePos& t) {
+            // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same dimensions
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        lo[e] = fminf(lo[e], __shfl_xor(lo[e], 16)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 16));
-        lo[e] = fminf(lo[e], __shfl_xor(lo[e], 32)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 32));
-    }
-    // lane row r writes the terms of heads r, r + 4, ...
-    const int c = lane & 15, r = lane >> 4;
-#pragma unroll
-    for (int h0 = 0; h0 < G; h0 += 4) {
-        const int h = h0 + r;
-        if (h < G) {
-            const u32x4_l qw = reinterpret_cast<const u32x4_l*>(
-                P.q + ((int64_t)b * P.num_q_heads + kvh * G + h) * kHeadDim)[c];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const double q0 = bf16_lo(qw[e]), q1 = bf16_hi(qw[e]);
-                terms[w][h][8 * c + 2 * e] = fmax(q0 * (double)lo[2 * e], q0 * (double)hi[2 * e]);
-                terms[w][h][8 * c + 2 * e + 1] = fmax(q1 * (double)lo[2 * e + 1], q1 * (double)hi[2 * e + 1]);
+            for (int e = 0; e < 8; ++e) {
+                lo[e] = fminf(lo[e], __shfl_xor(lo[e], 16)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 16));
+                lo[e] = fminf(lo[e], __shfl_xor(lo[e], 32)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 32));
             }
-        }
-    }
-    wave_lds_fence();
-    double s = -INFINITY;
-    if (lane < G) {
-        s = 0.0;
-        for (int d = 0; d < 128; ++d) s = s + terms[w][lane][d];
-    }
-    s = wave_max(s);
-    if (lane == 0) P.scores[(int64_t)gidx * P.max_blocks + blk] = s;
+            // lane row r writes the terms of heads r, r + 4, ...
+            const int c = lane & 15, r = lane >> 4;
+#pragma unroll
+            for (int h0 = 0; h0 < G; h0 += 4) {
+                const int h = h0 + r;
+                if (h < G) {
+                    const u32x4_l qw = reinterpret_cast<const u32x4_l*>(
+                        P.q + ((int64_t)t.b * P.num_q_heads + t.kvh * G + h) * kHeadDim)[c];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const double q0 = bf16_lo(qw[e]), q1 = bf16_hi(qw[e]);
+                        terms[w][h][8 * c + 2 * e] = fmax(q0 * (double)lo[2 * e], q0 * (double)hi[2 * e]);
+                        terms[w][h][8 * c + 2 * e + 1] = fmax(q1 * (double)lo[2 * e + 1], q1 * (double)hi[2 * e + 1]);
+                    }
+                }
+            }
+            wave_lds_fence();
+            double s = -INFINITY;
+            if (lane < G) {
+                s = 0.0;
+                for (int d = 0; d < 128; ++d) s = s + terms[w][lane][d];
+            }
+            s = wave_max(s);
+            if (lane == 0) P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = s;
+            wave_lds_fence();   // the terms are read before the next block writes them
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }
+        });
+}
+
+// A persistent launch of 256-thread workgroups: as many as are resident at
+// once (never more than one wavefront per work item), so that no workgroup
+// waits for another to finish before it starts its share.
+template <class Kernel>
+hipError_t launch_persistent(Kernel kernel, int64_t items, size_t lds, hipStream_t stream, const ListParams& P) {
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, lds);
+    if (e != hipSuccess) return e;
+    if (per_cu < 1) per_cu = 1;
+    const int64_t grid = std::min<int64_t>((items + 3) / 4, (int64_t)cus * per_cu);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), lds, stream, P);
+    return hipGetLastError();
 }
 
 // a before b: larger score, then smaller id
@@ -430,21 +512,22 @@ art_status art_build_block_list(const art_decode_shape* shape, const art_list_op
     P.list_len = block_list_len;
     P.scores = scores;
     const int groups = shape->batch * shape->num_kv_heads;
-    if (importance) {
+    if (importance && (int64_t)groups * mb > 0) {
         const int64_t waves = (int64_t)groups * mb;
-        const dim3 grid((unsigned)((waves + 3) / 4));
         if (opts->score_kind == ART_SCORE_KEY_NORM) {
-            hipLaunchKernelGGL(score_key_norm_kernel, grid, dim3(256), 4 * 32 * kRowPitch, stream, P);
+            if (launch_persistent(score_key_norm_kernel, waves, 4 * 32 * kRowPitch, stream, P) != hipSuccess)
+                return ART_ERR_HIP;
         } else {
+            hipError_t e;
             switch (shape->num_q_heads / shape->num_kv_heads) {
-                case 1: hipLaunchKernelGGL(score_query_bound_kernel<1>, grid, dim3(256), 0, stream, P); break;
-                case 2: hipLaunchKernelGGL(score_query_bound_kernel<2>, grid, dim3(256), 0, stream, P); break;
-                case 4: hipLaunchKernelGGL(score_query_bound_kernel<4>, grid, dim3(256), 0, stream, P); break;
-                case 8: hipLaunchKernelGGL(score_query_bound_kernel<8>, grid, dim3(256), 0, stream, P); break;
-                default: hipLaunchKernelGGL(score_query_bound_kernel<16>, grid, dim3(256), 0, stream, P); break;
+                case 1: e = launch_persistent(score_query_bound_kernel<1>, waves, 0, stream, P); break;
+                case 2: e = launch_persistent(score_query_bound_kernel<2>, waves, 0, stream, P); break;
+                case 4: e = launch_persistent(score_query_bound_kernel<4>, waves, 0, stream, P); break;
+                case 8: e = launch_persistent(score_query_bound_kernel<8>, waves, 0, stream, P); break;
+                default: e = launch_persistent(score_query_bound_kernel<16>, waves, 0, stream, P); break;
             }
+            if (e != hipSuccess) return ART_ERR_HIP;
         }
-        if (hipGetLastError() != hipSuccess) return ART_ERR_HIP;
     }
     const size_t lds = importance ? (size_t)sn * (sizeof(double) + sizeof(int)) +
                                         (kListThreads / 64 + 1) * sizeof(int)
