@@ -99,8 +99,9 @@ typedef struct {
  * patience = 1 is "no patience"; INT32_MAX runs the detector without ever
  * stopping.  chunk_blocks = 0 lets the library pick the split of each
  * traversal into chunks from the shape alone (never from the data or the
- * thresholds); 1..16 asks for that many blocks per chunk (capped at what
- * the shared-memory budget holds for the shape).  The chunking changes
+ * thresholds: four leading chunks of 3 blocks, then chunks of up to 9);
+ * 1..16 asks for that many blocks in every chunk (capped at what the
+ * shared-memory budget holds for the shape).  The chunking changes
  * rounding only.
  *
  * probe_stride chooses the probe x(t) = P o(t) that the stability test of

@@ -7,24 +7,27 @@
 // the patience counter of Eq. (3) and the early break of Algorithm 1.
 //
 // Work decomposition
-//   A group's traversal of T blocks is cut into chunks of C consecutive
-//   blocks.  The chunks of all groups form one chunk-major work list (chunk
-//   0 of every group, then chunk 1, ...).  The grid is persistent (as many
-//   workgroups as the chip holds); workgroups take list indices from one
-//   epoch-tagged queue word, so workgroups freed by groups that stopped early
-//   move on to the groups that stop late.  Indices are handed out in order,
-//   so a chunk only ever waits on chunks some workgroup already holds: no
-//   deadlock whatever the dispatch order.
+//   A group's traversal of T blocks is cut into chunks of consecutive
+//   blocks (with the default plan, four leading chunks of 3 blocks, then
+//   chunks of C).  The chunks of all groups form eight chunk-major work lists
+//   (list x holds the groups g with g mod 8 = x: chunk 0 of each, then chunk
+//   1, ...).  The grid is persistent (as many workgroups as the chip holds);
+//   workgroups take list indices from epoch-tagged queue words, so
+//   workgroups freed by groups that stopped early move on to the groups that
+//   stop late.  Each list is handed out in order and a chunk only waits on
+//   earlier chunks of its own group, so every wait targets a chunk that some
+//   workgroup already holds: no deadlock whatever the dispatch order.
 //
-//   Loaders (wavefronts 1..3): the leader claims a chunk when one of the LDS
-//   chunk buffers (two or three) is free; the loaders stream its 64-token tiles from HBM
+//   Loaders (wavefronts 1..3): the leader claims a chunk when one of the two
+//   LDS chunk buffers is free; the loaders stream its 64-token tiles from HBM
 //   (16-byte loads, four 64-byte row segments per K load instruction, four
 //   256-byte rows per V load instruction), compute the scores of all g query
-//   heads with v_mfma_f32_16x16x32_bf16 (query heads are the M rows, tokens
-//   the N columns, head dims the reduction), the tile softmax in base 2 with
-//   row reductions over DPP, and P.V on the VALU in fp32, and leave (m, l,
-//   sum p v) for each tile in LDS.  Chunks after an announced stop are not
-//   loaded.
+//   heads with v_mfma_f32_16x16x32_bf16 (tokens are the M rows, query heads
+//   the N columns, head dims the reduction), the tile softmax in base 2, and
+//   P.V on the same MFMA with P split into three bf16 parts (fp32 accuracy),
+//   and leave (m, l, sum p v) for each block in LDS.  Chunks after an
+//   announced stop are not loaded, and a loader gives up a chunk mid-way
+//   once a stop before it is announced.
 //
 //   Resolver (wavefront 0), per ready chunk:
 //     - folds the loaders' partials into the chunk aggregate;
@@ -37,12 +40,13 @@
 //       block (normalised running output o(t), increment d = o(t) - o(t-1),
 //       d_scale = |d|, d_direction = 1 - cos from |o|^2, |d|^2 and o.d
 //       without cancellation);
-//     - publishes a stability summary; if the chunk can hold the stop (or is
-//       the group's last chunk) it looks back the same way over the
-//       stability states (entering patience run, stop already found) and
-//       either stops inside the chunk (announces the stop so that later
-//       chunks skip their loads, then writes out/lse/stop_block) or, as the
-//       last chunk, writes the untruncated result.
+//     - publishes a stability summary, and announces "stop at or before this
+//       chunk" at once when the chunk's own blocks hold a run of p stable
+//       steps; if the chunk can hold the stop (or is the group's last chunk)
+//       it looks back the same way over the stability states (entering
+//       patience run, stop already found) and either stops inside the chunk
+//       (announces the stop, then writes out/lse/stop_block) or, as the last
+//       chunk, writes the untruncated result.
 //   Cross-workgroup data goes through the workspace with device-coherent
 //   accesses only, as the XCDs of MI355X have separate L2 caches (see the
 //   workspace helpers below).
