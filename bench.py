@@ -312,6 +312,26 @@ def main():
         torch.cuda.empty_cache()
         return res
 
+    # a measured ceiling beside the published one: a plain device copy of
+    # 1 GiB (read plus written bytes over its HIP-event time, median of 10)
+    def copy_rate_gbps():
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            dst.copy_(src)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        del src, dst
+        torch.cuda.empty_cache()
+        return 2 * (1 << 30) / (sorted(ts)[len(ts) // 2] * 1e-3) / 1e9
+
+    copy_gbps = copy_rate_gbps()
     on = measure(tau, phi, pat, args.steps, args.warmup)
     off = None if args.no_off else measure(0.0, phi, pat, max(5, args.steps // 2), max(2, args.warmup // 2))
     cpu = None if args.no_cpu else cpu_baseline(wl, eligible_tokens, tau, phi, pat, args.cpu_seconds)
@@ -323,8 +343,9 @@ def main():
         traffic = counted_traffic(args.workload, mode) if defaults else None
         return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": ach / HBM_PEAK_GBPS, "traffic": traffic,
-                "kernel": "art_decode_kernel<4>", "kernel_ms": r["kernel_ms"],
-                "alg_bytes_per_launch": r["alg_bytes_per_launch"]}
+                "kernel": f"art_decode_kernel<{spec.group_size}>", "kernel_ms": r["kernel_ms"],
+                "alg_bytes_per_launch": r["alg_bytes_per_launch"],
+                "measured_copy_gbps": copy_gbps, "frac_of_measured_copy": ach / copy_gbps}
 
     line = {
         "metric": "decode-attn KV tokens·heads/s; achieved HBM GB/s on bytes read; % KV blocks skipped",
