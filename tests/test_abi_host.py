@@ -213,3 +213,30 @@ def test_block_list_rejects_null_outputs_before_launch(lib):
     empty = _shape(batch=0, max_blocks_per_list=16)
     assert lib.art_build_block_list(ctypes.byref(empty), ctypes.byref(_lopts()), None, None, None,
                                     None, None, None, None, None, 0, None) == _lib.OK
+
+
+def test_size_limits_of_the_plan(lib):
+    """Traversals of 2^19 blocks and more do not fit the 19-bit stability runs
+    of the flag words: refused.  One block less is planned (the workspace is
+    sized from the shape alone, so no memory is needed to ask)."""
+    big = 1 << 19
+    n, st = _ws(_shape(batch=1, num_kv_heads=1, num_q_heads=4, max_pages_per_seq=big,
+                       num_pages=big), _opts())
+    assert (n, st) == (0, _lib.ERR_UNSUPPORTED)
+    n, st = _ws(_shape(batch=1, num_kv_heads=1, num_q_heads=4, max_pages_per_seq=big - 1,
+                       num_pages=big), _opts())
+    assert st == _lib.OK and n > 0
+    # a block list longer than any dense traversal sets the bound too
+    n, st = _ws(_shape(batch=1, num_kv_heads=1, num_q_heads=4, max_blocks_per_list=big), _opts())
+    assert (n, st) == (0, _lib.ERR_UNSUPPORTED)
+
+
+def test_work_list_must_fit_a_queue_word(lib):
+    """Chunks of all groups are numbered in 24 bits: a launch whose work list
+    would not fit (with any chunk size the LDS budget allows) is refused."""
+    n, st = _ws(_shape(batch=16384, num_kv_heads=8, num_q_heads=32, max_pages_per_seq=8192,
+                       num_pages=1 << 20), _opts())
+    assert (n, st) == (0, _lib.ERR_UNSUPPORTED)
+    n, st = _ws(_shape(batch=64, num_kv_heads=8, num_q_heads=32, max_pages_per_seq=8192,
+                       num_pages=1 << 20), _opts())
+    assert st == _lib.OK and n > 0
