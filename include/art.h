@@ -172,7 +172,10 @@ art_status art_workspace_init(void* workspace, size_t bytes, hipStream_t stream)
  *   lse          fp32 [batch][num_q_heads], natural log; -inf for T = 0.
  *   stop_block   int32 [batch][num_kv_heads]: blocks consumed t* (0..T).
  *   workspace    see art_decode_workspace_bytes / art_workspace_init.
- * Returns ART_OK once the work is enqueued.
+ * Returns ART_OK once the work is enqueued.  Each call tags the workspace
+ * with a fresh value of a host-side counter that is passed as a kernel
+ * argument, so a call captured in a HIP graph must not be replayed: a
+ * replay would reuse the captured tag.
  */
 art_status art_decode_attention(const art_decode_shape* shape, const art_decode_opts* opts,
                                 const void* q, const void* k_cache, const void* v_cache,
