@@ -831,6 +831,7 @@ __device__ void write_empty_wave(const KernelParams& P, int b, int kvh, int lane
 
 constexpr int kLoaders = kWaves - 1;   // wavefronts 1..3 stream tiles
 constexpr int kMaxSlots = 3;           // chunk buffers in LDS (the plan picks 2 or 3)
+constexpr int kLenCache = 256;         // sequence lengths kept in LDS
 enum SlotState : int { kSlotFree = 0, kSlotLoading = 1, kSlotReady = 2, kSlotEnd = 3 };
 // slot metadata words
 constexpr int kMetaSeq = 0, kMetaState = 1, kMetaGroup = 2, kMetaChunk = 3, kMetaDone = 4, kMetaAbort = 5;
@@ -1158,7 +1159,11 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   // the static block below is a multiple of 16 bytes
   extern __shared__ __align__(16) float smem[];
   __shared__ __align__(16) int s_meta[kMaxSlots][8];
-  static_assert(sizeof(int) * kMaxSlots * 8 % 16 == 0, "static LDS must keep the dynamic part aligned");
+  // lengths of the first kLenCache sequences: a dense traversal's claims
+  // need no round trip
+  __shared__ __align__(16) int s_len[kLenCache];
+  static_assert(sizeof(int) * (kMaxSlots * 8 + kLenCache) % 16 == 0,
+                "static LDS must keep the dynamic part aligned");
   constexpr int REC = Cfg<G>::REC;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int n_groups = P.batch * P.num_kv_heads;
@@ -1170,6 +1175,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   uint16_t* vbuf_all = reinterpret_cast<uint16_t*>(smem + ((n_slots * slot_floats + 3) & ~3));
 
   if (tid < kMaxSlots * 8) (&s_meta[0][0])[tid] = (tid % 8 == kMetaSeq) ? -1 : 0;
+  for (int i = tid; i < min(P.batch, kLenCache); i += kThreads) s_len[i] = P.seq_lens[i];
   __syncthreads();
 
   if (wave == 0) {
@@ -1232,16 +1238,19 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
           continue;
         }
         const int g = qx + kQueues * (i % nx), kh = i / nx;
-        // the group's lengths and stop word in one round trip
-        const int L_raw = P.seq_lens[g / P.num_kv_heads];
+        // the group's lengths (for a dense traversal of one of the first
+        // kLenCache sequences from LDS, with no round trip); the loaders
+        // check for a stop announced before the chunk with their page reads
+        const int bq = g / P.num_kv_heads;
+        const int L_raw = (bq < kLenCache && !P.block_list) ? lds_ld(&s_len[bq]) : P.seq_lens[bq];
         const int T_raw = raw_list_len(P, g);
-        const uint64_t sw = ld_relaxed(P.stop_word + g);
         const GroupInfo gi = group_info_raw(P, g, L_raw, T_raw);
         if (gi.n_chunks == 0) {
           if (kh == 0) write_empty_wave<G>(P, gi.b, gi.kvh, lane);
           continue;
         }
-        if (kh >= gi.n_chunks || stop_word_before(sw, P.epoch, kh)) continue;
+        if (kh >= gi.n_chunks) continue;
+        if (P.block_list && stop_word_before(ld_relaxed(P.stop_word + g), P.epoch, kh)) continue;
         gsel = g;
         ksel = kh;
         len_sel = L_raw;
@@ -1291,6 +1300,9 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       // tiles are fetched together once per chunk: lane 4m + n covers
       // 16-token group n of the wave's m-th tile (at most 16 tiles per wave).
       const int n_my = lw < nb ? (nb - lw + kLoaders - 1) / kLoaders * tpb : 0;
+      // the stop word travels with the page reads: a chunk that lies after
+      // an announced stop is given up before any tile is loaded
+      const uint64_t sw0 = ld_relaxed(P.stop_word + gidx);
       int my_tok0 = 0x7fffffff, my_page = 0;
       {
         const int m = lane >> 2, n = lane & 3;
@@ -1308,7 +1320,10 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
           if (my_tok0 < gi.L) my_page = clamp_page(P, gi.b, min(my_tok0 + 16 * n, gi.L - 1));
         }
       }
-      for (int m = 0; m < n_my; ++m) {
+      if (stop_word_before(sw0, P.epoch, k)) {
+        aborted = true;
+      }
+      for (int m = 0; m < n_my && !aborted; ++m) {
         const int i = lw + kLoaders * (m / tpb), j = m % tpb;
         // a stop announced by an earlier chunk makes this chunk's work moot;
         // the flag read here completes while the tile's loads are in flight
