@@ -77,20 +77,34 @@ constexpr int kRowPitch = 272;   // bytes per token row in the LDS tile (256 + 1
 // skipping blocks past their sequence's end, one 64-token tile at a time.
 // The loads of the next tile are issued before the current tile is
 // processed, and the page ids two tiles ahead before that, so that every
-// wavefront keeps one tile of keys in flight while it computes.
+// wavefront keeps one tile of keys in flight while it computes.  Two things
+// keep that overlap intact: every load is issued by every lane on every
+// path (addresses are clamped instead of branched around, so the compiler
+// can count the loads still in flight instead of waiting for all of them),
+// and the two tile buffers swap roles in an unrolled pair of steps instead
+// of being copied (a copy would wait for the next tile's loads).  The
+// sequence lengths of the first kListLenCache sequences are read from LDS.
+constexpr int kListLenCache = 256;
+
 struct TilePos {
     int64_t item;   // flattened group * max_blocks + block; >= n_items when done
     int gidx, b, kvh, blk, t0, j1;
 };
 
+__device__ __forceinline__ int cached_len(const ListParams& P, const int* s_len, int b) {
+    return b < kListLenCache ? s_len[b] : seq_len_of(P, b);
+}
+
 // The first tile of the first block at or after `item` that holds tokens.
-__device__ __forceinline__ TilePos first_tile(const ListParams& P, int64_t item, int64_t stride,
-                                              int64_t n_items) {
+__device__ __forceinline__ TilePos first_tile(const ListParams& P, const int* s_len, int64_t item,
+                                              int64_t stride, int64_t n_items) {
     TilePos t;
+    t.gidx = t.b = t.kvh = t.blk = t.t0 = 0;
+    t.j1 = 1;
     for (; item < n_items; item += stride) {
         const int gidx = (int)(item / P.max_blocks), blk = (int)(item % P.max_blocks);
         const int b = gidx / P.num_kv_heads;
-        const int L = seq_len_of(P, b);
+        const int L = cached_len(P, s_len, b);
         const int j0 = blk * P.block_size;
         if (j0 < L) {
             t.gidx = gidx; t.b = b; t.kvh = gidx % P.num_kv_heads; t.blk = blk;
@@ -102,34 +116,45 @@ __device__ __forceinline__ TilePos first_tile(const ListParams& P, int64_t item,
     return t;
 }
 
-__device__ __forceinline__ TilePos next_tile(const ListParams& P, TilePos t, int64_t stride, int64_t n_items) {
+__device__ __forceinline__ TilePos next_tile(const ListParams& P, const int* s_len, TilePos t,
+                                             int64_t stride, int64_t n_items) {
+    if (t.item >= n_items) return t;
     if (t.t0 + 64 < t.j1) {
         t.t0 += 64;
         return t;
     }
-    return first_tile(P, t.item + stride, stride, n_items);
+    return first_tile(P, s_len, t.item + stride, stride, n_items);
 }
 
-// Page of 16-token piece n of the tile, in lane n (n < 4).
-__device__ __forceinline__ int tile_pages(const ListParams& P, const TilePos& t, int lane) {
-    int pg = 0;
-    if (t.item >= 0 && lane < 4) {
-        const int tok = min(t.t0 + 16 * lane, t.j1 - 1);
-        pg = P.page_table[(int64_t)t.b * P.max_pages + (tok >> P.page_shift)];
-        pg = pg < 0 ? 0 : (pg >= P.num_pages ? P.num_pages - 1 : pg);
-    }
-    return pg;
+// Page of 16-token piece (lane & 3) of the tile, in lane n (n < 4).  Every
+// lane reads a valid entry; a tile past the end reads the first one.
+__device__ __forceinline__ int tile_pages(const ListParams& P, const TilePos& t, int64_t n_items,
+                                          int lane) {
+    const bool live = t.item < n_items;
+    const int tok = live ? min(t.t0 + 16 * (lane & 3), t.j1 - 1) : 0;
+    const int64_t at = live ? (int64_t)t.b * P.max_pages + (tok >> P.page_shift) : 0;
+    int pg = P.page_table[at];
+    return pg < 0 ? 0 : (pg >= P.num_pages ? P.num_pages - 1 : pg);
 }
 
-__device__ __forceinline__ void load_tile(const ListParams& P, const TilePos& t, int pages, int lane,
-                                          u32x4_l (&v)[kTileLoads]) {
+// Rows past the tile's end (and every row of a tile past the end of the
+// work) read the tile's first row again: they are ignored by the callers
+// and cost no memory traffic.
+__device__ __forceinline__ void load_tile(const ListParams& P, const TilePos& t, int pages, int64_t n_items,
+                                          int lane, u32x4_l (&v)[kTileLoads]) {
     const int pmask = (1 << P.page_shift) - 1;
+    const bool live = t.item < n_items;
 #pragma unroll
     for (int i = 0; i < kTileLoads; ++i) {
-        const int tok = t.t0 + 4 * i + (lane >> 4);
-        const int pg = __builtin_amdgcn_readlane(pages, i >> 2);
-        const uint16_t* row = P.k + pg * P.ks_page + t.kvh * P.ks_head + (int64_t)(tok & pmask) * P.ks_tok;
-        v[i] = tok < t.j1 ? reinterpret_cast<const u32x4_l*>(row)[lane & 15] : u32x4_l{0u, 0u, 0u, 0u};
+        int tok = t.t0 + 4 * i + (lane >> 4);
+        int pg = __builtin_amdgcn_readlane(pages, i >> 2);
+        if (tok >= t.j1) {
+            tok = t.t0;
+            pg = __builtin_amdgcn_readlane(pages, 0);
+        }
+        const uint16_t* row = live ? P.k + pg * P.ks_page + t.kvh * P.ks_head + (int64_t)(tok & pmask) * P.ks_tok
+                                   : P.k;
+        v[i] = reinterpret_cast<const u32x4_l*>(row)[lane & 15];
     }
 }
 
@@ -138,34 +163,48 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_wave_barrier();
 }
 
-// Walks this wavefront's tiles with the loads one tile ahead; `tile_fn(t, v)`
-// consumes a tile, `block_fn(t)` ends a block (after its last tile).
-template <class TileFn, class BlockFn>
-__device__ __forceinline__ void stream_tiles(const ListParams& P, TileFn tile_fn, BlockFn block_fn) {
+// Loads the lengths of the first kListLenCache sequences into LDS (every
+// thread of the workgroup takes part; a barrier follows).
+__device__ __forceinline__ void cache_lens(const ListParams& P, int* s_len) {
+    for (int i = threadIdx.x; i < min(P.batch, kListLenCache); i += blockDim.x) s_len[i] = seq_len_of(P, i);
+    __syncthreads();
+}
+
+// Walks this wavefront's tiles with the loads one tile ahead; `pre_fn(t)`
+// issues the loads that the current tile's `block_fn` will need (before the
+// next tile's keys, so that waiting for them does not wait for the keys),
+// `tile_fn(t, v)` consumes a tile, `block_fn(t)` ends a block (after its
+// last tile).
+template <class PreFn, class TileFn, class BlockFn>
+__device__ __forceinline__ void stream_tiles(const ListParams& P, const int* s_len, PreFn pre_fn,
+                                             TileFn tile_fn, BlockFn block_fn) {
     const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int64_t stride = (int64_t)gridDim.x * 4;
     const int64_t n_items = (int64_t)P.batch * P.num_kv_heads * P.max_blocks;
-    TilePos cur = first_tile(P, (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), stride, n_items);
+    TilePos cur = first_tile(P, s_len, (int64_t)blockIdx.x * 4 + wave, stride, n_items);
     if (cur.item >= n_items) return;
-    TilePos nxt = next_tile(P, cur, stride, n_items);
-    int pg_cur = tile_pages(P, cur, lane);
-    int pg_nxt = nxt.item < n_items ? tile_pages(P, nxt, lane) : 0;
-    u32x4_l v[kTileLoads];
-    load_tile(P, cur, pg_cur, lane, v);
-    for (;;) {
-        // two tiles ahead: its page ids; one tile ahead: its keys
-        const TilePos nn = nxt.item < n_items ? next_tile(P, nxt, stride, n_items) : nxt;
-        const int pg_nn = nn.item < n_items ? tile_pages(P, nn, lane) : 0;
-        u32x4_l w[kTileLoads];
-        if (nxt.item < n_items) load_tile(P, nxt, pg_nxt, lane, w);
-        tile_fn(cur, v);
+    TilePos nxt = next_tile(P, s_len, cur, stride, n_items);
+    const int pg_cur = tile_pages(P, cur, n_items, lane);
+    int pg_nxt = tile_pages(P, nxt, n_items, lane);
+    u32x4_l a[kTileLoads], b[kTileLoads];
+    load_tile(P, cur, pg_cur, n_items, lane, a);
+    // One step: the page ids two tiles ahead, the keys of the next tile into
+    // `nb`, then the current tile (in `cb`).  False once the work is done.
+    auto step = [&](u32x4_l (&cb)[kTileLoads], u32x4_l (&nb)[kTileLoads]) -> bool {
+        const TilePos nn = next_tile(P, s_len, nxt, stride, n_items);
+        const int pg_nn = tile_pages(P, nn, n_items, lane);
+        pre_fn(cur);
+        load_tile(P, nxt, pg_nxt, n_items, lane, nb);
+        tile_fn(cur, cb);
         if (nxt.item != cur.item) block_fn(cur);
-        if (nxt.item >= n_items) break;
-#pragma unroll
-        for (int i = 0; i < kTileLoads; ++i) v[i] = w[i];
+        if (nxt.item >= n_items) return false;
         cur = nxt;
         nxt = nn;
         pg_nxt = pg_nn;
+        return true;
+    };
+    while (step(a, b) && step(b, a)) {
     }
 }
 
@@ -173,10 +212,12 @@ __device__ __forceinline__ void stream_tiles(const ListParams& P, TileFn tile_fn
 // through LDS, 32 tokens at a time.
 __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P) {
     extern __shared__ __align__(16) unsigned char tiles[];
+    __shared__ __align__(16) int s_len[kListLenCache];
+    cache_lens(P, s_len);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     unsigned char* tile = tiles + w * 32 * kRowPitch;
     double best = -1.0;   // below any sum of squares
-    stream_tiles(P,
+    stream_tiles(P, s_len, [](const TilePos&) {},
         [&](const TilePos& t, const u32x4_l (&v)[kTileLoads]) {
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
@@ -205,8 +246,8 @@ __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P)
             }
         },
         [&](const TilePos& t) {
-            const double m = wave_max(best);
-            if (lane == 0) P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = m;
+            // every lane stores the same value (no branch around the store)
+            P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = wave_max(best);
             best = -1.0;
         });
 }
@@ -218,11 +259,25 @@ __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P)
 template <int G>
 __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams P) {
     __shared__ double terms[4][G][128];
+    __shared__ __align__(16) int s_len[kListLenCache];
+    cache_lens(P, s_len);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     float lo[8], hi[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }
-    stream_tiles(P,
+    // lane row r holds dimensions 8*(lane & 15) .. +7 of query heads r, r + 4, ...
+    constexpr int QR = (G + 3) / 4;
+    u32x4_l qw[QR];
+    const int c = lane & 15, r = lane >> 4;
+    stream_tiles(P, s_len,
+        [&](const TilePos& t) {
+#pragma unroll
+            for (int h0 = 0, u = 0; h0 < G; h0 += 4, ++u) {
+                const int h = min(h0 + r, G - 1);
+                qw[u] = reinterpret_cast<const u32x4_l*>(
+                    P.q + ((int64_t)t.b * P.num_q_heads + t.kvh * G + h) * kHeadDim)[c];
+            }
+        },
         [&](const TilePos& t, const u32x4_l (&v)[kTileLoads]) {
 #pragma unroll
             for (int i = 0; i < kTileLoads; ++i) {
@@ -244,16 +299,13 @@ __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams
                 lo[e] = fminf(lo[e], __shfl_xor(lo[e], 32)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 32));
             }
             // lane row r writes the terms of heads r, r + 4, ...
-            const int c = lane & 15, r = lane >> 4;
 #pragma unroll
-            for (int h0 = 0; h0 < G; h0 += 4) {
+            for (int h0 = 0, u = 0; h0 < G; h0 += 4, ++u) {
                 const int h = h0 + r;
                 if (h < G) {
-                    const u32x4_l qw = reinterpret_cast<const u32x4_l*>(
-                        P.q + ((int64_t)t.b * P.num_q_heads + t.kvh * G + h) * kHeadDim)[c];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const double q0 = bf16_lo(qw[e]), q1 = bf16_hi(qw[e]);
+                        const double q0 = bf16_lo(qw[u][e]), q1 = bf16_hi(qw[u][e]);
                         terms[w][h][8 * c + 2 * e] = fmax(q0 * (double)lo[2 * e], q0 * (double)hi[2 * e]);
                         terms[w][h][8 * c + 2 * e + 1] = fmax(q1 * (double)lo[2 * e + 1], q1 * (double)hi[2 * e + 1]);
                     }
@@ -265,8 +317,7 @@ __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams
                 s = 0.0;
                 for (int d = 0; d < 128; ++d) s = s + terms[w][lane][d];
             }
-            s = wave_max(s);
-            if (lane == 0) P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = s;
+            P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = wave_max(s);
             wave_lds_fence();   // the terms are read before the next block writes them
 #pragma unroll
             for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }

@@ -148,3 +148,19 @@ def test_full_size_importance_lists():
         _compare(wl, host, OL.IMPORTANCE, kind, 512, 1, True)
     del wl
     torch.cuda.empty_cache()
+
+
+def test_full_size_ragged_importance_lists():
+    """The ragged batch's shape: 32 sequences of 8K-64K tokens (many blocks
+    past each sequence's end), 8 KV heads of 8 query heads each."""
+    spec = W.WORKLOADS["qwen3_32b_ragged"]
+    _say(f"  generating {spec.name} on the device")
+    wl = W.make_workload(spec, device=DEV)
+    host = copy.copy(wl)
+    for name in ("q", "k_cache", "v_cache", "page_table", "seq_lens"):
+        setattr(host, name, getattr(wl, name).cpu())
+    max_blocks = (int(wl.page_table.shape[1]) * spec.page_size + spec.block_size - 1) // spec.block_size
+    for kind in (OL.KEY_NORM, OL.QUERY_BOUND):
+        _compare(wl, host, OL.IMPORTANCE, kind, max_blocks // 4, 1, True)
+    del wl, host
+    torch.cuda.empty_cache()
