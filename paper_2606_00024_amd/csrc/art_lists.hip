@@ -400,7 +400,11 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
         id[i] = i < n ? i : 0x7fffffff;
     }
     __syncthreads();
-    // bitonic sort; pair p of a stage compares positions i and i + stride
+    // Bitonic sort; pair p of a stage compares positions i and i + stride.
+    // Below a stride of 64 both positions of pair p lie in the 64-position
+    // segment p / 32, whose 32 pairs all belong to one wavefront (for every
+    // p = tid + k * kListThreads): those stages need no workgroup barrier,
+    // only the wavefront's own LDS accesses done before the next stage.
     for (int size = 2; size <= N; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
             for (int p = tid; p < N / 2; p += kListThreads) {
@@ -414,8 +418,12 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
                     id[i] = ij; id[j] = ii;
                 }
             }
-            __syncthreads();
+            if (stride >= 64) __syncthreads();
+            else wave_lds_fence();
         }
+        // the next size starts with a stride of 64 or more (positions of
+        // other wavefronts), or the selection below reads every position
+        if (size >= 64 || size == N) __syncthreads();
     }
     // forced blocks and the budget for the others
     const int ns = min(P.sink_blocks, n);
