@@ -76,6 +76,8 @@ CASES = [
     (64, 1, 2, 16, 3000, 64, 32),
     (65, 3, 1, 2, (0, 65, 5000), 256, 128),
     (66, 2, 3, 4, (1, 4097), 64, 64),
+    # more sequences than the score kernels keep lengths for in LDS (256)
+    (67, 300, 1, 4, tuple(int(x) for x in np.random.default_rng(8).integers(0, 700, 300)), 64, 16),
 ]
 SELECT = [(8, 1, True), (3, 0, False), (5, 4, True), (10 ** 4, 0, False), (0, 2, False)]
 

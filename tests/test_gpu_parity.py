@@ -95,6 +95,22 @@ def test_small_matrix(case, thr):
     assert rep.ok(), str(rep)
 
 
+# more sequences than the kernel keeps lengths for in LDS (256): sequences
+# past that read their lengths from memory
+MANY_LENS = tuple(int(x) for x in np.random.default_rng(7).integers(0, 700, 300))
+
+
+@pytest.mark.parametrize("lists", [False, True], ids=["dense", "lists"])
+@pytest.mark.parametrize("thr", THRESHOLDS[:3], ids=["cfg", "relaxed", "off"])
+def test_batch_beyond_the_length_cache(lists, thr):
+    wl = _small((12, 300, 1, 4, MANY_LENS, 64, 16, 0, lists))
+    tau, phi, p = thr
+    gpu = _run(wl, tau, phi, p)
+    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p)
+    _say("  ", rep)
+    assert rep.ok(), str(rep)
+
+
 @pytest.mark.parametrize("chunk", [1, 2, 3, 5, 16])
 def test_chunking_changes_rounding_only(chunk):
     wl = _small((11, 2, 2, 4, (3000, 2500), 64, 64, 0, False))
