@@ -341,11 +341,18 @@ def main():
     def roofline(r, mode):
         ach = r["hbm_gbps_on_bytes_read"]
         traffic = counted_traffic(args.workload, mode) if defaults else None
-        return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBPS, "traffic": traffic,
-                "kernel": f"art_decode_kernel<{spec.group_size}>", "kernel_ms": r["kernel_ms"],
-                "alg_bytes_per_launch": r["alg_bytes_per_launch"],
-                "measured_copy_gbps": copy_gbps, "frac_of_measured_copy": ach / copy_gbps}
+        out = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+               "frac": ach / HBM_PEAK_GBPS, "traffic": traffic,
+               "kernel": f"art_decode_kernel<{spec.group_size}>", "kernel_ms": r["kernel_ms"],
+               "alg_bytes_per_launch": r["alg_bytes_per_launch"],
+               "measured_copy_gbps": copy_gbps, "frac_of_measured_copy": ach / copy_gbps}
+        if traffic is not None:
+            # the rate at which the counted bytes (reads past each stop
+            # included) move: how busy HBM is, as opposed to how much of
+            # what it moves the result needs
+            out["traffic_gbps"] = traffic / (r["kernel_ms"] * 1e-3) / 1e9
+            out["traffic_frac"] = out["traffic_gbps"] / HBM_PEAK_GBPS
+        return out
 
     line = {
         "metric": "decode-attn KV tokens·heads/s; achieved HBM GB/s on bytes read; % KV blocks skipped",
