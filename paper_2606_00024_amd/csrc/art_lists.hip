@@ -137,9 +137,9 @@ __device__ __forceinline__ int tile_pages(const ListParams& P, const TilePos& t,
     return pg < 0 ? 0 : (pg >= P.num_pages ? P.num_pages - 1 : pg);
 }
 
-// Rows past the tile's end (and every row of a tile past the end of the
-// work) read the tile's first row again: they are ignored by the callers
-// and cost no memory traffic.
+// Rows past the tile's end read the tile's first row again, and every row
+// of a tile past the end of the work reads the pool's first row: the
+// callers ignore them, and they add no memory traffic beyond a line or two.
 __device__ __forceinline__ void load_tile(const ListParams& P, const TilePos& t, int pages, int64_t n_items,
                                           int lane, u32x4_l (&v)[kTileLoads]) {
     const int pmask = (1 << P.page_shift) - 1;
