@@ -70,8 +70,8 @@ def counted_traffic(workload, mode):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama3_8b_32k")
     ap.add_argument("--copies", type=int, default=4, help="KV pool copies rotated across steps")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -173,8 +173,10 @@ def time_steps(runner, steps, warmup):
         e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kern_ms = sum(e0.elapsed_time(e1) for e0, e1 in evs) / steps
-    return wall, kern_ms
+    per = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    time_steps.last = {"kernel_ms_p10": per[int(0.1 * (steps - 1))], "kernel_ms_p50": per[(steps - 1) // 2],
+                       "kernel_ms_p90": per[int(0.9 * (steps - 1))]}
+    return wall, sum(per) / steps
 
 
 def cpu_baseline(wl, eligible_tokens, tau, phi, patience, budget_s):
@@ -295,12 +297,14 @@ def main():
         run = Runner(wl, args.copies, t, f, p, args.chunk_blocks)
         print(f"[bench] timing tau={t} phi={f} p={p} steps={steps}", file=sys.stderr, flush=True)
         wall, kern_ms = time_steps(run, steps, warmup)
+        spread = dict(time_steps.last)
         alg, read_tokens, blocks = algorithmic_bytes(wl, run.stop)
         total_blocks = sum(map(sum, wl.traversal_lengths()))
         ms = wall / steps * 1e3
         res = {
             "ms_per_step": ms,
             "kernel_ms": kern_ms,
+            **spread,
             "effective_tokens_heads_per_s": eligible_tokens / (wall / steps),
             "read_tokens_heads_per_s": read_tokens / (wall / steps),
             "hbm_gbps_on_bytes_read": alg / (kern_ms * 1e-3) / 1e9,
@@ -374,6 +378,8 @@ def main():
         "skipped_pct": on["skipped_pct"],
         "read_tokens_heads_per_s": on["read_tokens_heads_per_s"],
         "kernel_ms": on["kernel_ms"],
+        "kernel_ms_p10": on["kernel_ms_p10"], "kernel_ms_p50": on["kernel_ms_p50"],
+        "kernel_ms_p90": on["kernel_ms_p90"],
         "roofline": roofline(on, "on"),
         "cpu_baseline": cpu,
         "termination_off": None if off is None else dict(off, roofline=roofline(off, "off")),
