@@ -400,16 +400,48 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
         id[i] = i < n ? i : 0x7fffffff;
     }
     __syncthreads();
-    // Bitonic sort; pair p of a stage compares positions i and i + stride.
-    // Below a stride of 64 both positions of pair p lie in the 64-position
-    // segment p / 32, whose 32 pairs all belong to one wavefront (for every
-    // p = tid + k * kListThreads): those stages need no workgroup barrier,
-    // only the wavefront's own LDS accesses done before the next stage.
-    for (int size = 2; size <= N; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+    // Bitonic sort of positions 0..N-1 (N a power of two) into descending
+    // score, ties by ascending id.  Stages with a stride of 64 or more go
+    // through LDS, one pair per thread and a workgroup barrier each.  Stages
+    // below a stride of 64 never leave a 64-position segment: they run in
+    // registers, each wavefront taking whole segments (lane l holds position
+    // 64 s + l) and exchanging with lane l ^ stride by shuffles, so that a
+    // segment is read and written once per run of such stages.  Sizes up to
+    // 64 have no other stages and run in a single pass.
+    const int wave = tid >> 6, lane = tid & 63;
+    auto segment_pass = [&](int size_from, int size_to) {
+        for (int seg = wave; seg * 64 < N; seg += kListThreads / 64) {
+            const int pos = seg * 64 + lane;
+            double k = pos < N ? key[pos] : -INFINITY;
+            int i = pos < N ? id[pos] : 0x7fffffff;
+            for (int size = size_from; size <= size_to; size <<= 1) {
+                const bool up = (pos & size) == 0;   // this run sorts "before" first
+                for (int stride = min(size >> 1, 32); stride > 0; stride >>= 1) {
+                    const double pk = __shfl_xor(k, stride);
+                    const int pi = __shfl_xor(i, stride);
+                    const bool lower = (lane & stride) == 0;
+                    const bool mine_first = before(k, i, pk, pi);
+                    // the lower position of an ascending-"before" run keeps
+                    // the element that comes first, the upper one the other
+                    if ((lower == up) != mine_first) {
+                        k = pk;
+                        i = pi;
+                    }
+                }
+            }
+            if (pos < N) {
+                key[pos] = k;
+                id[pos] = i;
+            }
+        }
+    };
+    segment_pass(2, min(N, 64));
+    __syncthreads();
+    for (int size = 128; size <= N; size <<= 1) {
+        for (int stride = size >> 1; stride >= 64; stride >>= 1) {
             for (int p = tid; p < N / 2; p += kListThreads) {
                 const int i = (p / stride) * 2 * stride + (p % stride), j = i + stride;
-                const bool up = (i & size) == 0;   // this run sorts "before" first
+                const bool up = (i & size) == 0;
                 const double ki = key[i], kj = key[j];
                 const int ii = id[i], ij = id[j];
                 const bool swap = up ? before(kj, ij, ki, ii) : before(ki, ii, kj, ij);
@@ -418,12 +450,10 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
                     id[i] = ij; id[j] = ii;
                 }
             }
-            if (stride >= 64) __syncthreads();
-            else wave_lds_fence();
+            __syncthreads();
         }
-        // the next size starts with a stride of 64 or more (positions of
-        // other wavefronts), or the selection below reads every position
-        if (size >= 64 || size == N) __syncthreads();
+        segment_pass(size, size);
+        __syncthreads();
     }
     // forced blocks and the budget for the others
     const int ns = min(P.sink_blocks, n);
