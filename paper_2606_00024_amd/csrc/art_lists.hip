@@ -421,8 +421,9 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
                     const int pi = __shfl_xor(i, stride);
                     const bool lower = (lane & stride) == 0;
                     const bool mine_first = before(k, i, pk, pi);
-                    // the lower position of an ascending-"before" run keeps
-                    // the element that comes first, the upper one the other
+                    // in a run that puts "before" first, the lower position
+                    // keeps whichever element comes first and the upper one
+                    // the other; the other runs the other way round
                     if ((lower == up) != mine_first) {
                         k = pk;
                         i = pi;
