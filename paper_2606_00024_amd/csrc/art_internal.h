@@ -19,8 +19,8 @@ constexpr int kMaxChunkBlocks = 16;  // blocks per chunk
 // hands out at most its list length plus one final index per workgroup.
 constexpr int kQueueBits = 24;
 constexpr int64_t kQueueSlack = 1 << 16;
-// The work list is split over this many queue words (groups g with
-// g % kQueues == x go to queue x), each in its own 256-byte line.
+// The work list is split over this many queue words (each run of kQueues
+// groups spread over all of them), each in its own 256-byte line.
 constexpr int kQueues = 8;
 constexpr int kQueueStride = 32;  // uint64 words between queue words
 

@@ -10,8 +10,9 @@
 //   A group's traversal of T blocks is cut into chunks of consecutive
 //   blocks (with the default plan, four leading chunks of 3 blocks, then
 //   chunks of C).  The chunks of all groups form eight chunk-major work lists
-//   (list x holds the groups g with g mod 8 = x: chunk 0 of each, then chunk
-//   1, ...).  The grid is persistent (as many workgroups as the chip holds);
+//   (list x holds the groups 8r + (x + r) mod 8 of every full run r of eight
+//   groups, and the leftover groups g with g mod 8 = x: chunk 0 of each, then
+//   chunk 1, ...).  The grid is persistent (as many workgroups as the chip holds);
 //   workgroups take list indices from epoch-tagged queue words, so
 //   workgroups freed by groups that stopped early move on to the groups that
 //   stop late.  Each list is handed out in order and a chunk only waits on
@@ -845,8 +846,9 @@ __device__ __forceinline__ void lds_st(int* p, int v) {
 }
 
 // Work queues.  The chunks of the launch form kQueues chunk-major lists:
-// queue x holds the groups g with g % kQueues == x (n_x of them), and its
-// index i stands for chunk i / n_x of group x + kQueues * (i % n_x).  Each
+// queue x holds n_x groups, and its index i stands for chunk i / n_x of
+// group x + kQueues * (i % n_x), rotated within its run of kQueues groups
+// (see the claim).  Each
 // list is handed out from its own workspace word (call epoch << 24 | next
 // index) by one fetch-and-add (claim_issue; claim_finish decodes it), so
 // that claims spread over kQueues atomic units.  A word left by an earlier
@@ -1237,7 +1239,14 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
           qx = (qx + 1) % kQueues;
           continue;
         }
-        const int g = qx + kQueues * (i % nx), kh = i / nx;
+        int g = qx + kQueues * (i % nx);
+        const int kh = i / nx;
+        // Within every full run of kQueues groups, rotate by the run's
+        // index, so that each list mixes KV heads instead of holding one
+        // head's groups of every sequence (whose stops can fall close
+        // together and leave one list's workgroups with the late work).
+        // A bijection per list: every group still belongs to one list.
+        if (g / kQueues < n_groups / kQueues) g = (g / kQueues) * kQueues + (g % kQueues + g / kQueues) % kQueues;
         // the group's lengths (for a dense traversal of one of the first
         // kLenCache sequences from LDS, with no round trip); the loaders
         // check for a stop announced before the chunk with their page reads
