@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 5
+#define ART_ABI_VERSION 6
 
 typedef enum {
     ART_OK = 0,
@@ -134,6 +134,9 @@ typedef struct {
                                       the probe options are ignored): full attention over
                                       the traversal, stop_block = T; the baseline that
                                       shows what the test itself costs */
+    int32_t max_wait_polls;        /* 0 = default (2^22 polls of about a microsecond each);
+                                      n > 0: a wait on another workgroup's chunk gives up
+                                      after n polls (a watchdog; see art_workspace_status) */
 } art_decode_opts;
 
 /* Version of this ABI (ART_ABI_VERSION). */
@@ -204,6 +207,13 @@ art_status art_validate_inputs(const art_decode_shape* shape, const art_decode_o
  * since its initialisation gave up waiting on a predecessor chunk (a bounded
  * spin that ends the kernel instead of hanging it).  *device_status receives
  * ART_OK or ART_ERR_DEVICE_TIMEOUT.
+ *
+ * Every wait of the decode kernel is bounded (max_wait_polls).  The first
+ * wave that gives up records the call in the workspace's error word; every
+ * other wait of that call then ends within a few polls, so the launch
+ * drains promptly.  The outputs of such a call are unspecified (some groups
+ * may be left unwritten).  The error stays recorded until the workspace is
+ * initialised again; later calls on the workspace run normally.
  */
 art_status art_workspace_status(const void* workspace, size_t workspace_bytes,
                                 hipStream_t stream, int32_t* device_status);

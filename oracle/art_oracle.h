@@ -71,8 +71,10 @@ enum {
 /*
  * q, k_cache, v_cache: bf16 bit patterns (host memory).
  * block_list / block_list_len: NULL for the dense traversal.
- * force_stop: NULL, or [batch][num_kv_heads]; a value f >= 1 makes group
- *   (b, kvh) stop after step min(f, T) regardless of the criterion.
+ * force_stop: NULL, or [batch][num_kv_heads] (with per_head_stop:
+ *   [batch][num_q_heads], one value per query head); a value f >= 1 makes
+ *   group (b, kvh) (or that query head) stop after step min(f, T)
+ *   regardless of the criterion.
  * group_mask: NULL, or [batch][num_kv_heads]; groups with 0 are skipped
  *   (their outputs are left untouched).
  * out [batch][num_q_heads][head_dim], lse [batch][num_q_heads] (fp64),

@@ -41,7 +41,7 @@ class DecodeShape(ctypes.Structure):
 
 
 # ART_ABI_VERSION of include/art.h that these structure layouts follow
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 
 class DecodeOpts(ctypes.Structure):
@@ -49,7 +49,8 @@ class DecodeOpts(ctypes.Structure):
                 ("phi", ctypes.c_float), ("patience", ctypes.c_int32),
                 ("dense_order", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
                 ("chunk_blocks", ctypes.c_int32), ("probe_stride", ctypes.c_int32),
-                ("scale_of_accumulator", ctypes.c_int32), ("no_detector", ctypes.c_int32)]
+                ("scale_of_accumulator", ctypes.c_int32), ("no_detector", ctypes.c_int32),
+                ("max_wait_polls", ctypes.c_int32)]
 
 
 class ListOpts(ctypes.Structure):

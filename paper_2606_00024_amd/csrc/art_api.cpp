@@ -74,7 +74,7 @@ art_status check_shape(const art_decode_shape* s, const art_decode_opts* o) {
         (o->probe_stride & (o->probe_stride - 1)) != 0 ||
         (o->probe_stride > 1 && s->head_dim % o->probe_stride != 0) ||
         (o->scale_of_accumulator != 0 && o->scale_of_accumulator != 1) ||
-        (o->no_detector != 0 && o->no_detector != 1))
+        (o->no_detector != 0 && o->no_detector != 1) || o->max_wait_polls < 0)
         return ART_ERR_INVALID_ARG;
     const int g = s->num_q_heads / s->num_kv_heads;
     if (s->head_dim != art::kHeadDim) return ART_ERR_UNSUPPORTED;
@@ -174,7 +174,7 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
 
     art::WorkspaceLayout& w = p->ws;
     size_t off = 0;
-    w.error_off = off;      off = align_up(off + 4);
+    w.error_off = off;      off = align_up(off + 8);
     w.queue_off = off;      off = align_up(off + 8 * art::kQueueStride * art::kQueues);
     w.stop_off = off;       off = align_up(off + 8 * (size_t)n_groups);
     w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
@@ -293,13 +293,13 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.lse = lse;
     k.stop_block = stop_block;
     char* ws = static_cast<char*>(workspace);
-    k.error_word = reinterpret_cast<uint32_t*>(ws + plan.ws.error_off);
+    k.error_word = reinterpret_cast<uint64_t*>(ws + plan.ws.error_off);
     k.queue = reinterpret_cast<uint64_t*>(ws + plan.ws.queue_off);
     k.stop_word = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_off);
     k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
     k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
     k.epoch = next_epoch();
-    k.spin_limit = kSpinLimit;
+    k.spin_limit = opts->max_wait_polls > 0 ? (uint32_t)opts->max_wait_polls : kSpinLimit;
     if (k.epoch >= (uint64_t(1) << 40)) return ART_ERR_UNSUPPORTED;
     return art::launch_decode(plan, k, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
 }
@@ -367,10 +367,10 @@ art_status art_validate_inputs(const art_decode_shape* shape, const art_decode_o
 
 art_status art_workspace_status(const void* workspace, size_t workspace_bytes, hipStream_t stream,
                                 int32_t* device_status) {
-    if (!workspace || workspace_bytes < 4 || !device_status) return ART_ERR_INVALID_ARG;
-    uint32_t word = 0;
+    if (!workspace || workspace_bytes < 8 || !device_status) return ART_ERR_INVALID_ARG;
+    uint64_t word = 0;
     if (hipStreamSynchronize(stream) != hipSuccess) return ART_ERR_HIP;
-    if (hipMemcpy(&word, workspace, 4, hipMemcpyDeviceToHost) != hipSuccess) return ART_ERR_HIP;
+    if (hipMemcpy(&word, workspace, 8, hipMemcpyDeviceToHost) != hipSuccess) return ART_ERR_HIP;
     *device_status = word == 0 ? ART_OK : ART_ERR_DEVICE_TIMEOUT;
     return ART_OK;
 }

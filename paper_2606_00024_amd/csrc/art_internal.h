@@ -37,7 +37,7 @@ enum ChunkState : uint32_t {
 
 // Byte layout of a workspace (all offsets from its start, 256-aligned).
 struct WorkspaceLayout {
-    size_t error_off;        // uint32 error word
+    size_t error_off;        // uint64 error word: 0, or epoch << 8 | status of the call that gave up
     size_t queue_off;        // kQueues work-queue words (one per 256 bytes): epoch << 24 | next index
     size_t stop_off;         // uint64 [groups] announced stop: epoch << 24 | chunk
     size_t flags_off;        // uint64 [groups][max_chunks]: epoch << 24 | state << 20 | payload
@@ -93,7 +93,7 @@ struct KernelParams {
     float* lse;
     int32_t* stop_block;
     // workspace
-    uint32_t* error_word;
+    uint64_t* error_word;
     uint64_t* queue;
     uint64_t* stop_word;
     uint64_t* flags;

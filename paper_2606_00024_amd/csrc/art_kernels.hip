@@ -173,6 +173,35 @@ __device__ __forceinline__ uint32_t flag_state(uint64_t v, uint64_t epoch) {
 }
 __device__ __forceinline__ uint32_t flag_payload(uint64_t v) { return (uint32_t)(v & 0xfffffu); }
 
+// Bounded waits.  A wave that polls spin_limit times without seeing what it
+// waits for gives up: it stores this call's epoch and the timeout status in
+// the error word and ends.  Every other wait of the launch reads the error
+// word every kErrPollEvery polls and ends as soon as it carries this call's
+// epoch, so one give-up drains the whole grid within a few polls per wave
+// instead of each dependent wait spinning out its own limit.  (A word left
+// by an earlier call carries another epoch: it is reported by the status
+// call but does not end this one.)
+constexpr uint32_t kTimeoutStatus = 6u;   // ART_ERR_DEVICE_TIMEOUT
+constexpr uint32_t kErrPollEvery = 16u;
+template <typename Params>
+__device__ __forceinline__ void raise_timeout(const Params& P) {
+  __hip_atomic_store(P.error_word, (P.epoch << 8) | kTimeoutStatus, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename Params>
+__device__ __forceinline__ bool launch_failed(const Params& P) {
+  return (ld_relaxed(P.error_word) >> 8) == P.epoch;
+}
+// The give-up test of one poll of a wait loop (spin counts the polls made).
+template <typename Params>
+__device__ __forceinline__ bool wait_expired(const Params& P, uint32_t spin) {
+  if (spin >= P.spin_limit) {
+    raise_timeout(P);
+    return true;
+  }
+  return (spin % kErrPollEvery) == kErrPollEvery - 1 && launch_failed(P);
+}
+
 template <int G>
 struct Cfg {
   static constexpr int HPL = G >= 4 ? G / 4 : 1;   // head slots per lane (state layout)
@@ -660,10 +689,7 @@ __device__ int lookback_scan(const KernelParams& P, int gidx, int me, uint32_t n
       continue;
     }
     if (stop_announced_before(P, gidx, me)) return -2;
-    if (++it >= P.spin_limit) {
-      __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return -2;
-    }
+    if (wait_expired(P, ++it)) return -2;
     __builtin_amdgcn_s_sleep(2);
   }
   return -1;
@@ -708,21 +734,27 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
       continue;
     }
     if (stop_announced_before(P, gidx, me)) return false;
-    if (++it >= P.spin_limit) {
-      __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return false;
-    }
+    if (wait_expired(P, ++it)) return false;
     __builtin_amdgcn_s_sleep(2);
   }
-  // the state of chunk j (none when j = -1), then the summaries after it,
-  // 64 per read
+  // the state of chunk j (none when j = -1), then the chunks after it, 64
+  // per read.  The scan saw every one of them at least at its summary, but
+  // each read here may find a chunk that has meanwhile published its own
+  // stability state, whose payload replaced the summary in the flag word.
+  // Such a state is the fold over every chunk up to it, so the fold restarts
+  // from it: the same exact integer result either way.
   x = StabState{0, 0, 0, 0};
   if (j >= 0) x = unpack_stab(flag_payload(ld_relaxed(flags + j)));
   for (int i0 = j + 1; i0 < me; i0 += 64) {
     const int n = min(64, me - i0);
-    const uint32_t pl = lane < n ? flag_payload(ld_relaxed(flags + i0 + lane)) : 0u;
-    for (int u = 0; u < n; ++u)
-      x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), chunk_start(P, i0 + u), P.patience);
+    const uint64_t v = lane < n ? ld_relaxed(flags + i0 + lane) : 0ull;
+    const uint32_t pl = flag_payload(v);
+    const uint64_t is_state = __ballot(lane < n && flag_state(v, P.epoch) >= kStabInclusive);
+    for (int u = 0; u < n; ++u) {
+      const uint32_t w = __builtin_amdgcn_readlane(pl, u);
+      if ((is_state >> u) & 1ull) x = unpack_stab(w);
+      else x = stab_fold(x, unpack_summary(w), chunk_start(P, i0 + u), P.patience);
+    }
   }
   return true;
 }
@@ -890,8 +922,7 @@ __device__ int claim_finish(const KernelParams& P, int x, uint64_t v, int lane) 
           q = 0;
           break;
         }
-        if (spin >= P.spin_limit) {
-          __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (wait_expired(P, spin)) {
           q = 0x7fffffff;
           break;
         }
@@ -1189,10 +1220,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       for (uint32_t spin = 0;; ++spin) {
         st = lds_ld(&s_meta[slot][kMetaState]);
         if (lds_ld(&s_meta[slot][kMetaSeq]) == it && (st == kSlotReady || st == kSlotEnd)) break;
-        if (spin >= P.spin_limit) {
-          __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          return;
-        }
+        if (wait_expired(P, spin)) return;
         __builtin_amdgcn_s_sleep(1);
       }
       if (st == kSlotEnd) return;
@@ -1223,8 +1251,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       // leader: wait for the buffer, then claim the next chunk of the list
       bool gave_up = false;
       for (uint32_t spin = 0; lds_ld(&s_meta[slot][kMetaState]) != kSlotFree; ++spin) {
-        if (spin >= P.spin_limit) {
-          __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (wait_expired(P, spin)) {
           gave_up = true;  // hand out the end marker below
           break;
         }
@@ -1266,7 +1293,9 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         list_sel = T_raw;
         break;
       }
-      if (lane == 0) {
+      // (after a give-up the buffer may still be in the resolver's hands:
+      // only the end marker is handed out, its other words stay untouched)
+      if (lane == 0 && !gave_up) {
         lds_st(&s_meta[slot][kMetaGroup], gsel);
         lds_st(&s_meta[slot][kMetaChunk], ksel);
         lds_st(&s_meta[slot][kMetaLen], len_sel);
@@ -1285,10 +1314,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
     for (uint32_t spin = 0;; ++spin) {
       st = lds_ld(&s_meta[slot][kMetaState]);
       if (lds_ld(&s_meta[slot][kMetaSeq]) == it && (st == kSlotLoading || st == kSlotEnd)) break;
-      if (spin >= P.spin_limit) {
-        __hip_atomic_store(P.error_word, 6u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
-      }
+      if (wait_expired(P, spin)) return;
       __builtin_amdgcn_s_sleep(1);
     }
     if (st == kSlotEnd) return;

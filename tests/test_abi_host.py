@@ -93,7 +93,7 @@ def test_shape_errors(lib, kw, status):
     dict(out_dtype=5), dict(chunk_blocks=-1), dict(chunk_blocks=17),
     dict(softmax_scale=float("inf")), dict(probe_stride=-1), dict(probe_stride=3),
     dict(probe_stride=6), dict(probe_stride=256), dict(scale_of_accumulator=2),
-    dict(no_detector=-1), dict(no_detector=2),
+    dict(no_detector=-1), dict(no_detector=2), dict(max_wait_polls=-1),
 ])
 def test_option_errors(lib, kw):
     n, st = _ws(_shape(), _opts(**kw))
@@ -146,6 +146,20 @@ def test_decode_rejects_small_workspace(lib):
 
 def test_list_needs_row_stride(lib):
     assert _call(_shape(max_blocks_per_list=0), _opts(), dict(bl=16, bll=16)) == _lib.ERR_INVALID_ARG
+
+
+def test_launch_failure_is_reported_as_hip_error(lib):
+    """A call that passes every host check but whose launch fails returns
+    ART_ERR_HIP.  Forced here by the absence of a GPU; on a machine with one
+    the placeholder pointers would really be launched, so the test is skipped
+    there."""
+    if os.path.exists("/dev/kfd"):
+        pytest.skip("a GPU is visible: this test launches with placeholder pointers")
+    assert _call(_shape(), _opts()) == _lib.ERR_HIP
+    assert _call(_shape(), _opts(max_wait_polls=3)) == _lib.ERR_HIP
+    assert lib.art_workspace_init(16, 256, None) == _lib.ERR_HIP
+    dev = ctypes.c_int32(-1)
+    assert lib.art_workspace_status(16, 256, None, ctypes.byref(dev)) == _lib.ERR_HIP
 
 
 def test_empty_batch_is_a_no_op(lib):

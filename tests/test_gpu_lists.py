@@ -134,7 +134,7 @@ def test_device_lists_drive_the_decode_call():
         _say(f"  gpu call: decode over device lists tau={tau}")
         gpu = api.decode_workload(wl, tau=tau, phi=phi, patience=p)
         torch.cuda.synchronize()
-        rep = compare_workload(host, gpu, tau=tau, phi=phi, patience=p)
+        rep = compare_workload(host, gpu, tau=tau, phi=phi, patience=p, name="device_lists")
         _say("  ", rep)
         assert rep.ok(), str(rep)
 

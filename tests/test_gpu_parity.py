@@ -16,7 +16,7 @@ import torch
 
 import oracle
 from helpers import random_lists, small_workload
-from parity import Report, compare_sampled, compare_workload
+from parity import compare_workload, host_copy
 from paper_2606_00024_amd import _lib, api, workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -90,7 +90,7 @@ def test_small_matrix(case, thr):
     wl = _small(case)
     tau, phi, p = thr
     gpu = _run(wl, tau, phi, p)
-    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p)
+    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, name="small_matrix")
     _say("  ", rep)
     assert rep.ok(), str(rep)
 
@@ -106,7 +106,7 @@ def test_batch_beyond_the_length_cache(lists, thr):
     wl = _small((12, 300, 1, 4, MANY_LENS, 64, 16, 0, lists))
     tau, phi, p = thr
     gpu = _run(wl, tau, phi, p)
-    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p)
+    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, name="batch_300")
     _say("  ", rep)
     assert rep.ok(), str(rep)
 
@@ -116,7 +116,7 @@ def test_chunking_changes_rounding_only(chunk):
     wl = _small((11, 2, 2, 4, (3000, 2500), 64, 64, 0, False))
     for thr in [(1e-3, 1e-4, 5), (0.05, 1e-3, 2), (0.0, 1e-4, 5)]:
         gpu = _run(wl, *thr, chunk_blocks=chunk)
-        rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2])
+        rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2], name="chunking")
         _say("  ", chunk, thr, rep)
         assert rep.ok(), str(rep)
 
@@ -153,7 +153,7 @@ def test_empty_inputs_and_shared_lists():
     wl = small_workload(15, batch=3, kv_heads=2, group=4, seq_len=(0, 1000, 64), needles=2)
     _to_dev(wl)
     gpu = _run(wl, 1e-3, 1e-4, 5)
-    rep = compare_workload(wl, gpu, tau=1e-3, phi=1e-4, patience=5)
+    rep = compare_workload(wl, gpu, tau=1e-3, phi=1e-4, patience=5, name="empty_inputs")
     assert rep.ok(), str(rep)
     assert gpu[2][0].tolist() == [0, 0]
     # one list per sequence shared by its KV heads; one empty list
@@ -234,7 +234,7 @@ def test_workspace_reuse_across_shapes():
     for case in [SMALL[0], SMALL[3], SMALL[5], SMALL[0]]:
         wl = _small(case)
         gpu = _run(wl, 1e-3, 1e-4, 5, workspace=ws)
-        rep = compare_workload(wl, gpu, tau=1e-3, phi=1e-4, patience=5)
+        rep = compare_workload(wl, gpu, tau=1e-3, phi=1e-4, patience=5, name="workspace_reuse")
         assert rep.ok(), str(rep)
     assert api.workspace_status(ws) == _lib.OK
 
@@ -248,43 +248,112 @@ def test_workspace_reuse_through_every_layout():
         for case in SMALL:
             wl = _small(case)
             gpu = _run(wl, *thr, workspace=ws)
-            rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2])
+            rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2], name="workspace_layouts")
             assert rep.ok(), f"case s{case[0]} thr {thr}: {rep}"
     assert api.workspace_status(ws) == _lib.OK
 
 
 # ------------------------------------------------------------ full-size workloads
+# Every group of every workload at its real size is compared with the oracle
+# (fp64, OpenMP over the groups, on one host copy of the workload).  The
+# modes: the workload's thresholds and termination off; the ragged batch
+# runs its threshold sweep (including the paper's tau = 1e-5, phi = 1e-3).
 
-def _sample_groups(wl, n, seed):
-    s = wl.spec
-    rng = np.random.default_rng(seed)
-    all_g = [(b, h) for b in range(s.batch) for h in range(s.num_kv_heads)]
-    idx = rng.choice(len(all_g), size=min(n, len(all_g)), replace=False)
-    return sorted(all_g[i] for i in idx)
-
-
-FULL = [("tiny_4k", 2), ("llama3_8b_32k", 6), ("sparse25_128k", 6), ("qwen3_32b_ragged", 6),
-        ("long_512k", 3)]
-
-
-@pytest.mark.parametrize("name,nsample", FULL, ids=[f[0] for f in FULL])
-def test_full_size(name, nsample):
+def _full_modes(name):
     spec = W.WORKLOADS[name]
-    _say(f"  generating {name} on {DEV}")
-    wl = W.make_workload(spec, device=DEV)
-    torch.cuda.synchronize()
-    groups = _sample_groups(wl, nsample, spec.seed)
-    modes = [(spec.tau, spec.phi, spec.patience), (0.0, spec.phi, spec.patience)]
     if name == "qwen3_32b_ragged":
-        modes = [(t, f, spec.patience) for t, f in W.RAGGED_SWEEP] + [(0.0, 1e-4, 5)]
-    for tau, phi, p in modes:
-        gpu = _run(wl, tau, phi, p)
-        rep = compare_sampled(wl, gpu, groups, tau=tau, phi=phi, patience=p)
-        skipped = 1 - gpu[2].sum().item() / sum(map(sum, wl.traversal_lengths()))
-        _say(f"   {name} tau={tau} phi={phi}: {rep}  skipped={skipped:.3f}")
+        return [(t, f, spec.patience) for t, f in W.RAGGED_SWEEP] + [(0.0, 1e-4, 5)]
+    return [(spec.tau, spec.phi, spec.patience), (0.0, spec.phi, spec.patience)]
+
+
+FULL_CASES = [(n, m) for n in ("tiny_4k", "llama3_8b_32k", "sparse25_128k", "qwen3_32b_ragged",
+                               "long_512k") for m in _full_modes(n)]
+_FULL = {}
+
+
+def _full_workload(name):
+    """The workload on the GPU and its host copy, kept while the tests of
+    one workload run (they are consecutive)."""
+    if name not in _FULL:
+        _FULL.clear()
+        torch.cuda.empty_cache()
+        _say(f"  generating {name} on {DEV}")
+        wl = W.make_workload(W.WORKLOADS[name], device=DEV)
+        torch.cuda.synchronize()
+        _say(f"  host copy of {name}")
+        _FULL[name] = (wl, host_copy(wl))
+    return _FULL[name]
+
+
+@pytest.mark.parametrize("name,mode", FULL_CASES,
+                         ids=[f"{n}-tau{m[0]:g}-phi{m[1]:g}" for n, m in FULL_CASES])
+def test_full_size(name, mode):
+    wl, host = _full_workload(name)
+    tau, phi, p = mode
+    gpu = _run(wl, tau, phi, p)
+    rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, host=host, name=f"full:{name}")
+    skipped = 1 - gpu[2].sum().item() / sum(map(sum, wl.traversal_lengths()))
+    _say(f"   {name} tau={tau} phi={phi}: {rep}  skipped={skipped:.3f}")
+    assert rep.ok(), str(rep)
+    assert rep.groups == wl.spec.batch * wl.spec.num_kv_heads
+    if (name, mode) == FULL_CASES[-1] or FULL_CASES[FULL_CASES.index((name, mode)) + 1][0] != name:
+        _FULL.clear()
+        torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------ look-back stress
+# One chunk per block and long traversals: a chunk that can hold the stop
+# looks back over more than 64 chunks for the nearest stability state while
+# the chunks in between publish theirs.  Thresholds are picked from the
+# oracle's trajectory so that stability is intermittent and the stop falls
+# deep into each traversal.
+
+def _intermittent_tau(wl, patience, lo_frac=0.3):
+    """tau (phi = inf) that puts the most groups' oracle stops past lo_frac
+    of their traversal and before its end (None if it puts none there)."""
+    lens = np.asarray(wl.traversal_lengths())
+    Tm = int(lens.max())
+    r = oracle.decode_workload(wl, tau=0.0, phi=math.inf, patience=parity_no_stop(), trace_steps=Tm)
+    with np.errstate(invalid="ignore"):
+        worst = np.max(r["trace"][..., 0], axis=-1)  # [B][Hkv][T]: max d_scale over heads
+    from parity import reachable_stops
+    fin = worst[np.isfinite(worst)]
+    # thresholds far above fp32 rounding of the outputs only
+    cands = [t for t in np.quantile(fin, np.linspace(0.1, 0.95, 69)) if t >= 1e-4]
+    best, best_n = None, 0
+    for tau in cands:
+        n = 0
+        for b in range(lens.shape[0]):
+            for h in range(lens.shape[1]):
+                T = int(lens[b, h])
+                cls = (worst[b, h, :T] < tau).astype(np.int8)
+                cls[0] = 0  # step 1 is never stable
+                st = min(reachable_stops(cls, patience))
+                n += int(lo_frac * T <= st < T)
+        if n > best_n:
+            best, best_n = float(tau), n
+    return best
+
+
+def parity_no_stop():
+    from parity import NO_STOP
+    return NO_STOP
+
+
+@pytest.mark.parametrize("seed,g,p", [(35, 4, 6), (40, 4, 6), (39, 8, 5), (41, 8, 5)])
+def test_lookback_stress_one_block_chunks(seed, g, p):
+    wl = small_workload(seed, batch=2, kv_heads=2, group=g, seq_len=(24000, 20000), needles=6)
+    tau = _intermittent_tau(wl, p)
+    if tau is None:
+        pytest.skip("no threshold puts every stop deep into its traversal for this seed")
+    _to_dev(wl)
+    host = host_copy(wl)
+    for rep_i in range(4):
+        gpu = _run(wl, tau, math.inf, p, chunk_blocks=1)
+        rep = compare_workload(wl, gpu, tau=tau, phi=math.inf, patience=p, host=host,
+                               name="lookback_stress")
+        _say(f"   stress g={g} p={p} tau={tau:.3e} run {rep_i}: {rep} stops={gpu[2].tolist()}")
         assert rep.ok(), str(rep)
-    del wl
-    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[f"s{c[0]}" for c in SMALL])
@@ -298,6 +367,6 @@ def test_no_detector_is_full_attention(case):
     torch.cuda.synchronize()
     T = np.asarray(wl.traversal_lengths())
     assert np.array_equal(gpu[2].cpu().numpy(), T)
-    rep = compare_workload(wl, gpu, tau=0.0, phi=1e-4, patience=5)
+    rep = compare_workload(wl, gpu, tau=0.0, phi=1e-4, patience=5, name="no_detector")
     _say("  ", rep)
     assert rep.ok(), str(rep)

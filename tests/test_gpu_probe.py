@@ -15,7 +15,7 @@ import torch
 
 import oracle
 from helpers import random_lists, small_workload, uniform_key_case
-from parity import compare_sampled, compare_workload
+from parity import compare_workload, host_copy
 from paper_2606_00024_amd import _lib, api, workloads as W
 from paper_2606_00024_amd.agreement import classify
 
@@ -71,7 +71,8 @@ def test_probe_matrix(case, stride):
         _say(f"  gpu call: probe s{seed} stride={stride} tau={tau} phi={phi} p={p}")
         gpu = api.decode_workload(wl, tau=tau, phi=phi, patience=p, probe_stride=stride)
         torch.cuda.synchronize()
-        rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, probe_stride=stride)
+        rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, probe_stride=stride,
+                               name="probe_matrix")
         _say("  ", rep)
         assert rep.ok(), str(rep)
 
@@ -133,22 +134,22 @@ def test_probe_stride_one_is_the_whole_output():
     torch.cuda.synchronize()
 
 
-def test_probe_full_size_sampled():
+def test_probe_full_size_every_group():
     spec = W.WORKLOADS["llama3_8b_32k"]
     _say(f"  generating {spec.name} on {DEV}")
     wl = W.make_workload(spec, device=DEV)
     torch.cuda.synchronize()
-    rng = np.random.default_rng(7)
-    all_g = [(b, h) for b in range(spec.batch) for h in range(spec.num_kv_heads)]
-    groups = sorted(all_g[i] for i in rng.choice(len(all_g), size=5, replace=False))
+    host = host_copy(wl)
     for tau, phi, p in [(spec.tau, spec.phi, spec.patience), (1e-5, 1e-3, 5)]:
         _say(f"  gpu call: {spec.name} probe_stride=4 tau={tau} phi={phi}")
         gpu = api.decode_workload(wl, tau=tau, phi=phi, patience=p, probe_stride=4)
         torch.cuda.synchronize()
-        rep = compare_sampled(wl, gpu, groups, tau=tau, phi=phi, patience=p, probe_stride=4)
+        rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, probe_stride=4, host=host,
+                               name="full:probe4")
         _say("  ", rep)
         assert rep.ok(), str(rep)
-    del wl
+        assert rep.groups == spec.batch * spec.num_kv_heads
+    del wl, host
     torch.cuda.empty_cache()
 
 
@@ -201,7 +202,8 @@ def test_accumulator_reading_matrix(case):
                                       scale_of_accumulator=True)
             torch.cuda.synchronize()
             rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, probe_stride=stride,
-                                   scale_of_accumulator=True, tau_rel=ACC_TAU_REL)
+                                   scale_of_accumulator=True, tau_rel=ACC_TAU_REL,
+                                   name="accumulator")
             _say("  ", rep)
             assert rep.ok(), str(rep)
 
