@@ -185,47 +185,14 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     return ART_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-int32_t art_abi_version(void) { return ART_ABI_VERSION; }
-
-const char* art_status_str(int32_t status) {
-    switch (status) {
-        case ART_OK: return "ART_OK";
-        case ART_ERR_INVALID_ARG: return "ART_ERR_INVALID_ARG";
-        case ART_ERR_UNSUPPORTED: return "ART_ERR_UNSUPPORTED";
-        case ART_ERR_WORKSPACE_TOO_SMALL: return "ART_ERR_WORKSPACE_TOO_SMALL";
-        case ART_ERR_HIP: return "ART_ERR_HIP";
-        case ART_ERR_BAD_INDEX: return "ART_ERR_BAD_INDEX";
-        case ART_ERR_DEVICE_TIMEOUT: return "ART_ERR_DEVICE_TIMEOUT";
-        default: return "ART_ERR_UNKNOWN";
-    }
-}
-
-size_t art_decode_workspace_bytes(const art_decode_shape* shape, const art_decode_opts* opts,
-                                  int32_t* status) {
-    Plan p;
-    art_status st = make_plan(shape, opts, &p);
-    if (status) *status = st;
-    return st == ART_OK ? p.ws.total : 0;
-}
-
-art_status art_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
-    if (!workspace && bytes) return ART_ERR_INVALID_ARG;
-    if (bytes % 4) return ART_ERR_INVALID_ARG;
-    return art::launch_fill_zero(workspace, bytes, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
-}
-
-art_status art_decode_attention(const art_decode_shape* shape, const art_decode_opts* opts,
-                                const void* q, const void* k_cache, const void* v_cache,
-                                const int32_t* page_table, const int32_t* seq_lens,
-                                const int32_t* block_list, const int32_t* block_list_len,
-                                void* out, float* lse, int32_t* stop_block,
-                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    Plan plan;
-    art_status st = make_plan(shape, opts, &plan);
+// Host checks of a decode call and its plan (everything but the workspace).
+art_status check_decode_call(const art_decode_shape* shape, const art_decode_opts* opts,
+                             const void* q, const void* k_cache, const void* v_cache,
+                             const int32_t* page_table, const int32_t* seq_lens,
+                             const int32_t* block_list, const int32_t* block_list_len,
+                             const void* out, const float* lse, const int32_t* stop_block,
+                             Plan* plan) {
+    art_status st = make_plan(shape, opts, plan);
     if (st != ART_OK) return st;
     if (shape->batch == 0) return ART_OK;
     if (!q || !k_cache || !v_cache || !page_table || !seq_lens || !out || !lse || !stop_block)
@@ -234,9 +201,17 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     if (block_list && shape->max_blocks_per_list <= 0) return ART_ERR_INVALID_ARG;
     if (((uintptr_t)q | (uintptr_t)k_cache | (uintptr_t)v_cache | (uintptr_t)out) % 16)
         return ART_ERR_UNSUPPORTED;
-    if (!workspace || workspace_bytes < plan.ws.total) return ART_ERR_WORKSPACE_TOO_SMALL;
-    if ((uintptr_t)workspace % 8) return ART_ERR_INVALID_ARG;
+    return ART_OK;
+}
 
+// Kernel parameters of a checked call over the workspace at `workspace`,
+// then the launch.
+art_status enqueue_decode(const Plan& plan, const art_decode_shape* shape,
+                          const art_decode_opts* opts, const void* q, const void* k_cache,
+                          const void* v_cache, const int32_t* page_table,
+                          const int32_t* seq_lens, const int32_t* block_list,
+                          const int32_t* block_list_len, void* out, float* lse,
+                          int32_t* stop_block, void* workspace, hipStream_t stream) {
     KernelParams k;
     memset(&k, 0, sizeof k);
     k.batch = shape->batch;
@@ -302,6 +277,56 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
     k.spin_limit = opts->max_wait_polls > 0 ? (uint32_t)opts->max_wait_polls : kSpinLimit;
     if (k.epoch >= (uint64_t(1) << 40)) return ART_ERR_UNSUPPORTED;
     return art::launch_decode(plan, k, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t art_abi_version(void) { return ART_ABI_VERSION; }
+
+const char* art_status_str(int32_t status) {
+    switch (status) {
+        case ART_OK: return "ART_OK";
+        case ART_ERR_INVALID_ARG: return "ART_ERR_INVALID_ARG";
+        case ART_ERR_UNSUPPORTED: return "ART_ERR_UNSUPPORTED";
+        case ART_ERR_WORKSPACE_TOO_SMALL: return "ART_ERR_WORKSPACE_TOO_SMALL";
+        case ART_ERR_HIP: return "ART_ERR_HIP";
+        case ART_ERR_BAD_INDEX: return "ART_ERR_BAD_INDEX";
+        case ART_ERR_DEVICE_TIMEOUT: return "ART_ERR_DEVICE_TIMEOUT";
+        default: return "ART_ERR_UNKNOWN";
+    }
+}
+
+size_t art_decode_workspace_bytes(const art_decode_shape* shape, const art_decode_opts* opts,
+                                  int32_t* status) {
+    Plan p;
+    art_status st = make_plan(shape, opts, &p);
+    if (status) *status = st;
+    return st == ART_OK ? p.ws.total : 0;
+}
+
+art_status art_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
+    if (!workspace && bytes) return ART_ERR_INVALID_ARG;
+    if (bytes % 4) return ART_ERR_INVALID_ARG;
+    return art::launch_fill_zero(workspace, bytes, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
+}
+
+
+art_status art_decode_attention(const art_decode_shape* shape, const art_decode_opts* opts,
+                                const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* page_table, const int32_t* seq_lens,
+                                const int32_t* block_list, const int32_t* block_list_len,
+                                void* out, float* lse, int32_t* stop_block,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    Plan plan;
+    art_status st = check_decode_call(shape, opts, q, k_cache, v_cache, page_table, seq_lens,
+                                      block_list, block_list_len, out, lse, stop_block, &plan);
+    if (st != ART_OK || shape->batch == 0) return st;
+    if (!workspace || workspace_bytes < plan.ws.total) return ART_ERR_WORKSPACE_TOO_SMALL;
+    if ((uintptr_t)workspace % 8) return ART_ERR_INVALID_ARG;
+    return enqueue_decode(plan, shape, opts, q, k_cache, v_cache, page_table, seq_lens,
+                          block_list, block_list_len, out, lse, stop_block, workspace, stream);
 }
 
 art_status art_validate_inputs(const art_decode_shape* shape, const art_decode_opts* opts,
