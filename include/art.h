@@ -189,6 +189,37 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
                                 hipStream_t stream);
 
 /*
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * decode call (same kernels, same plan, bit-identical results) with the
+ * library's own scratch in place of the caller's workspace: a static device
+ * array of ART_STATIC_SCRATCH_BYTES per GPU, held from the library's first
+ * use on that GPU until the process ends.  The call allocates nothing; on
+ * its first use on a device (the current device) it takes the array's
+ * address and zero-fills it on `stream`.
+ *   - Arguments as for art_decode_attention, without the workspace.
+ *   - A shape whose art_decode_workspace_bytes() exceeds
+ *     ART_STATIC_SCRATCH_BYTES returns ART_ERR_WORKSPACE_TOO_SMALL before
+ *     anything is launched.
+ *   - Every call on one GPU shares that GPU's array: calls that overlap on a
+ *     GPU (different streams, or host threads issuing concurrently) race.
+ *     Order them, for example on one stream.
+ *   - Each call tags what it leaves in the array with a fresh value of the
+ *     call counter, so nothing needs clearing between calls (as for a
+ *     workspace), and a captured call must not be replayed.
+ *   - Bounded waits end the launch as in art_decode_attention; the error
+ *     word lives in the array and is not reported by this call.
+ */
+#define ART_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+art_status art_decode_attention_static(const art_decode_shape* shape, const art_decode_opts* opts,
+                                       const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* page_table, const int32_t* seq_lens,
+                                       const int32_t* block_list, const int32_t* block_list_len,
+                                       void* out, float* lse, int32_t* stop_block,
+                                       hipStream_t stream);
+
+/*
  * Checked mode: synchronously copies the index arrays to the host and checks
  * seq_lens (0 <= L <= max_pages_per_seq * page_size), the page ids each
  * sequence uses (0 <= id < num_pages), and the block lists (ids in range,

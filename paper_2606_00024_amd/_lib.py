@@ -23,7 +23,9 @@ OUT_BF16 = 1
 # every symbol include/art.h declares
 EXPORTS = ("art_abi_version", "art_status_str", "art_decode_workspace_bytes",
            "art_workspace_init", "art_decode_attention", "art_validate_inputs",
-           "art_workspace_status", "art_block_list_workspace_bytes", "art_build_block_list")
+           "art_workspace_status", "art_block_list_workspace_bytes", "art_build_block_list",
+           "art_decode_attention_static")
+STATIC_SCRATCH_BYTES = 64 << 20   # ART_STATIC_SCRATCH_BYTES
 
 LIST_IMPORTANCE = 0
 LIST_STREAMING = 1
@@ -92,6 +94,10 @@ def load() -> ctypes.CDLL:
         lib.art_decode_attention.argtypes = [
             ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts),
             vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        lib.art_decode_attention_static.restype = ctypes.c_int
+        lib.art_decode_attention_static.argtypes = [
+            ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts),
+            vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.art_validate_inputs.restype = ctypes.c_int
         lib.art_validate_inputs.argtypes = [
             ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts), vp, vp, vp, vp, vp,
@@ -142,6 +148,15 @@ def decode_attention(shape, opts, q, k, v, page_table, seq_lens, block_list, blo
         ctypes.byref(shape), ctypes.byref(opts), q, k, v, page_table, seq_lens,
         block_list or None, block_list_len or None, out, lse, stop_block,
         workspace or None, workspace_bytes, stream or None))
+
+
+def decode_attention_static(shape, opts, q, k, v, page_table, seq_lens, block_list,
+                            block_list_len, out, lse, stop_block, stream) -> int:
+    """Raw call of the variant over the library's static scratch (no
+    workspace); pointers are ints (0 for NULL).  Returns the status."""
+    return int(load().art_decode_attention_static(
+        ctypes.byref(shape), ctypes.byref(opts), q, k, v, page_table, seq_lens,
+        block_list or None, block_list_len or None, out, lse, stop_block, stream or None))
 
 
 def validate_inputs(shape, opts, page_table, seq_lens, block_list, block_list_len, stream):

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libart.so")
-SOURCES = ["art_kernels.hip", "art_lists.hip", "art_api.cpp"]
+SOURCES = ["art_kernels.hip", "art_lists.hip", "art_static.hip", "art_api.cpp"]
 ARCH = os.environ.get("ART_OFFLOAD_ARCH", "gfx950")
 
 

@@ -329,6 +329,23 @@ art_status art_decode_attention(const art_decode_shape* shape, const art_decode_
                           block_list, block_list_len, out, lse, stop_block, workspace, stream);
 }
 
+art_status art_decode_attention_static(const art_decode_shape* shape, const art_decode_opts* opts,
+                                       const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* page_table, const int32_t* seq_lens,
+                                       const int32_t* block_list, const int32_t* block_list_len,
+                                       void* out, float* lse, int32_t* stop_block,
+                                       hipStream_t stream) {
+    Plan plan;
+    art_status st = check_decode_call(shape, opts, q, k_cache, v_cache, page_table, seq_lens,
+                                      block_list, block_list_len, out, lse, stop_block, &plan);
+    if (st != ART_OK || shape->batch == 0) return st;
+    if (plan.ws.total > ART_STATIC_SCRATCH_BYTES) return ART_ERR_WORKSPACE_TOO_SMALL;
+    void* scratch = nullptr;
+    if (art::static_scratch(stream, &scratch) != (int)hipSuccess) return ART_ERR_HIP;
+    return enqueue_decode(plan, shape, opts, q, k_cache, v_cache, page_table, seq_lens,
+                          block_list, block_list_len, out, lse, stop_block, scratch, stream);
+}
+
 art_status art_validate_inputs(const art_decode_shape* shape, const art_decode_opts* opts,
                                const int32_t* page_table, const int32_t* seq_lens,
                                const int32_t* block_list, const int32_t* block_list_len,

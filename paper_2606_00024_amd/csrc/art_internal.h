@@ -105,5 +105,9 @@ struct KernelParams {
 // Launchers (art_kernels.hip).  Return a hipError_t.
 int launch_decode(const Plan& plan, const KernelParams& params, hipStream_t stream);
 int launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+// Device address of the library's static scratch on the current device
+// (art_static.hip); set up (address taken, zero-filled on `stream`) on the
+// first call per device.  Returns a hipError_t.
+int static_scratch(hipStream_t stream, void** ptr);
 
 }  // namespace art

@@ -162,6 +162,41 @@ def test_launch_failure_is_reported_as_hip_error(lib):
     assert lib.art_workspace_status(16, 256, None, ctypes.byref(dev)) == _lib.ERR_HIP
 
 
+def _call_static(shape, opts, ptrs=None):
+    p = dict(q=16, k=16, v=16, pt=16, sl=16, bl=0, bll=0, out=16, lse=16, stop=16)
+    if ptrs:
+        p.update(ptrs)
+    return _lib.decode_attention_static(shape, opts, p["q"], p["k"], p["v"], p["pt"], p["sl"],
+                                        p["bl"], p["bll"], p["out"], p["lse"], p["stop"], 0)
+
+
+def test_static_variant_checks_before_launch(lib):
+    """The variant over the library's static scratch takes the decode call's
+    host checks, and rejects a shape whose workspace exceeds the scratch
+    before anything is set up or launched."""
+    assert _call_static(_shape(), _opts(), dict(q=0)) == _lib.ERR_INVALID_ARG
+    assert _call_static(_shape(), _opts(tau=float("nan"))) == _lib.ERR_INVALID_ARG
+    assert _call_static(_shape(head_dim=64), _opts()) == _lib.ERR_UNSUPPORTED
+    assert _call_static(_shape(batch=0), _opts(), dict(q=0, k=0, v=0)) == _lib.OK
+    # 256 groups x 1024 blocks of g = 8: about 260 MB of chunk records
+    big = _shape(batch=32, num_q_heads=64, num_kv_heads=8, num_pages=40000,
+                 max_pages_per_seq=1024, k_stride_page=8 * 64 * 128, v_stride_page=8 * 64 * 128)
+    n, st = _ws(big, _opts())
+    assert st == _lib.OK and n > _lib.STATIC_SCRATCH_BYTES
+    assert _call_static(big, _opts()) == _lib.ERR_WORKSPACE_TOO_SMALL
+    n, st = _ws(_shape(), _opts())
+    assert st == _lib.OK and n <= _lib.STATIC_SCRATCH_BYTES
+    with open(os.path.join(ROOT, "include", "art.h")) as f:
+        m = re.search(r"#define ART_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", f.read())
+    assert int(m.group(1)) << int(m.group(2)) == _lib.STATIC_SCRATCH_BYTES
+
+
+def test_static_variant_launch_failure_is_reported(lib):
+    if os.path.exists("/dev/kfd"):
+        pytest.skip("a GPU is visible: this test launches with placeholder pointers")
+    assert _call_static(_shape(), _opts()) == _lib.ERR_HIP
+
+
 def test_empty_batch_is_a_no_op(lib):
     assert _call(_shape(batch=0), _opts(), dict(q=0, k=0, v=0)) == _lib.OK
 
