@@ -1,22 +1,25 @@
 #!/usr/bin/env python3
 """Benchmark: ART decode attention on one MI355X.
 
-A step is one call of art_decode_attention (the whole path: block loads,
+A step is one call of art_decode_attention: the whole path (block loads,
 scores, online softmax, P.V, the per-block stability test, patience and the
-early exit) on the Llama-3-8B-shaped decode layer: batch 8, 32 query / 8 KV
-heads, head_dim 128, 32768 cached tokens per sequence, KV block 64, paged KV
-(page 64, pages permuted in one pool), recency-first order, tau = 1e-3,
-phi = 1e-4, patience 5.  Inputs are resident in HBM; the KV pool is rotated
-over several identical copies so that consecutive steps do not hit in the
-256 MB last-level cache.
+early exit) over one decode step of a workload.  The headline workload is
+the Qwen3-32B-shaped ragged batch: 32 sequences of U{8192..65536} cached
+tokens, 64 query / 8 KV heads, head_dim 128, KV block 64, paged KV (page 64,
+pages permuted in one pool), recency-first order, tau = phi = 1e-3 (the
+middle of the swept thresholds), patience 5.  Inputs are resident in HBM;
+workloads smaller than a GiB rotate over several identical KV copies so that
+consecutive steps do not hit the 256 MB last-level cache.
 
 Prints one JSON line.  ``value`` is the effective KV tokens*heads/s: tokens
 of the traversal set (the whole cache, skipped blocks included) times KV
-heads, divided by wall time per step.  The line also carries the rate on
-tokens actually read, HBM GB/s on bytes read, the fraction of KV blocks
-skipped, the same figures with termination off (tau = 0: the detector runs
-every block and never fires), the roofline of the kernel and the CPU oracle
-timed on a bounded sample.
+heads, divided by wall time per step.  The line also carries the rate on the
+tokens actually read, HBM GB/s on the bytes the result needs, the fraction
+of KV blocks skipped, the distance of the output from full attention, the
+same figures with termination off (tau = 0: the test runs on every block and
+never fires), the threshold sweep, the other workloads, the roofline of the
+kernel against the published 8 TB/s and against the read ceiling measured in
+the same process, and the CPU oracle timed on bounded samples.
 """
 from __future__ import annotations
 
@@ -32,16 +35,19 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, published
+HEADLINE = "qwen3_32b_ragged"
+# the ragged batch's thresholds: the middle of the swept set (tau = phi)
+HEADLINE_THRESHOLDS = {"qwen3_32b_ragged": (1e-3, 1e-3)}
 
 # HBM bytes per launch of the decode kernel counted by rocprofv3 (FETCH_SIZE
 # scaled by 2.0 plus WRITE_SIZE scaled by 1.0: the factors a plain 1 GiB
-# device copy gives for those counters), per workload and mode at the
-# workload's default thresholds.  They hold only for the sources they were
-# counted on, identified by SHA-256; after any change to those sources the
-# figure is reported as null until it is counted again.
+# device copy gives for those counters), per workload, thresholds and mode.
+# They hold only for the sources they were counted on, identified by
+# SHA-256; after any change to those sources the figure is reported as null
+# until it is counted again.
 COUNTED_TRAFFIC = {
-    "sources_sha256": "374e8816aebcec613912408d86293f6d71e1dfcffed62373d7b7235212b9fefa",
-    "bytes": {("llama3_8b_32k", "on"): 541698816, ("llama3_8b_32k", "off"): 1120224000},
+    "sources_sha256": "",
+    "bytes": {},
 }
 TRAFFIC_SOURCES = ("art_kernels.hip", "art_api.cpp", "art_internal.h")
 
@@ -61,10 +67,10 @@ def sources_digest():
     return h.hexdigest()
 
 
-def counted_traffic(workload, mode):
+def counted_traffic(key):
     if sources_digest() != COUNTED_TRAFFIC["sources_sha256"]:
         return None
-    return COUNTED_TRAFFIC["bytes"].get((workload, mode))
+    return COUNTED_TRAFFIC["bytes"].get(key)
 
 
 def parse():
@@ -72,15 +78,21 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="llama3_8b_32k")
-    ap.add_argument("--copies", type=int, default=4, help="KV pool copies rotated across steps")
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--copies", type=int, default=0,
+                    help="KV pool copies rotated across steps (0: enough for 1 GiB, at most 8)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-off", action="store_true", help="skip the termination-off run")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the threshold sweep, the other workloads and the read ceiling")
+    ap.add_argument("--only-headline", action="store_true",
+                    help="time the headline mode only (for profiling the same launches)")
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--phi", type=float, default=None)
     ap.add_argument("--patience", type=int, default=None)
     ap.add_argument("--chunk-blocks", type=int, default=0)
+    ap.add_argument("--no-detector", action="store_true",
+                    help="the headline mode without the stability test (full attention)")
     ap.add_argument("--list-producer", action="store_true",
                     help="measure the device-side traversal-list producer (block scores and "
                          "selection) on the workload's shape instead of the decode step")
@@ -90,25 +102,40 @@ def parse():
     return ap.parse_args()
 
 
-class Runner:
-    """Pre-marshalled calls of the C ABI on torch's current stream."""
+def thresholds(spec, args=None):
+    tau, phi = HEADLINE_THRESHOLDS.get(spec.name, (spec.tau, spec.phi))
+    pat = spec.patience
+    if args is not None:
+        tau = tau if args.tau is None else args.tau
+        phi = phi if args.phi is None else args.phi
+        pat = pat if args.patience is None else args.patience
+    return tau, phi, pat
 
-    def __init__(self, wl, copies, tau, phi, patience, chunk_blocks):
+
+class Runner:
+    """Pre-marshalled calls of the C ABI on torch's current stream.  Every
+    call of a timed run writes its own stop_block buffer, so that the run
+    can check afterwards that every call stopped every group alike."""
+
+    def __init__(self, wl, copies, tau, phi, patience, chunk_blocks, no_detector=False,
+                 n_stop_bufs=1):
         import torch
         from paper_2606_00024_amd import _lib, api
         self._lib = _lib
+        self.api = api
         s = wl.spec
         self.wl = wl
         self.shape = api.make_shape(wl.q, wl.k_cache, wl.v_cache, wl.page_table,
                                     block_size=s.block_size, block_list=wl.block_list)
         self.opts = api.make_opts(softmax_scale=s.softmax_scale, tau=tau, phi=phi,
                                   patience=patience, dense_order=s.dense_order,
-                                  chunk_blocks=chunk_blocks)
+                                  chunk_blocks=chunk_blocks, no_detector=no_detector)
         dev = wl.q.device
         B, Hq, D = wl.q.shape
         self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
         self.lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-        self.stop = torch.empty((B, s.num_kv_heads), dtype=torch.int32, device=dev)
+        self.stops = torch.full((max(1, n_stop_bufs), B, s.num_kv_heads), -1, dtype=torch.int32,
+                                device=dev)
         self.ws_bytes = api.workspace_bytes(self.shape, self.opts)
         self.ws = api.new_workspace(self.ws_bytes, dev)
         self.pools = [(wl.k_cache, wl.v_cache)] + [
@@ -116,18 +143,38 @@ class Runner:
         self.stream = torch.cuda.current_stream(dev).cuda_stream
         p = lambda t: 0 if t is None else int(t.data_ptr())
         self.args = [(p(wl.q), p(k), p(v), p(wl.page_table), p(wl.seq_lens), p(wl.block_list),
-                      p(wl.block_list_len), p(self.out), p(self.lse), p(self.stop))
-                     for k, v in self.pools]
+                      p(wl.block_list_len), p(self.out), p(self.lse)) for k, v in self.pools]
+        self.stop_ptrs = [int(self.stops[i].data_ptr()) for i in range(self.stops.shape[0])]
         self.ws_ptr = int(self.ws.data_ptr())
         self.i = 0
 
-    def step(self):
+    @property
+    def stop(self):
+        return self.stops[0]
+
+    def step(self, buf=0):
         a = self.args[self.i % len(self.args)]
         self.i += 1
-        st = self._lib.decode_attention(self.shape, self.opts, *a, self.ws_ptr,
+        st = self._lib.decode_attention(self.shape, self.opts, *a, self.stop_ptrs[buf], self.ws_ptr,
                                         self.ws.numel(), self.stream)
         if st != 0:
             raise self._lib.ArtError(st, "art_decode_attention")
+
+    def check(self, n_bufs):
+        """After a timed run: no wait gave up, and every call left the same
+        stop_block (a call whose kernel gave up would not)."""
+        status = self.api.workspace_status(self.ws)
+        if status != self._lib.OK:
+            raise RuntimeError(f"timed run: workspace status {self._lib.status_str(status)}")
+        import torch
+        st = self.stops[:n_bufs]
+        if not bool((st == st[0]).all()) or bool((st[0] < 0).any()):
+            raise RuntimeError("timed run: stop_block differs between calls")
+
+
+def default_copies(wl):
+    pool = (wl.k_cache.numel() + wl.v_cache.numel()) * 2
+    return max(1, min(8, math.ceil((1 << 30) / max(pool, 1))))
 
 
 def algorithmic_bytes(wl, stop):
@@ -160,49 +207,181 @@ def algorithmic_bytes(wl, stop):
 
 
 def time_steps(runner, steps, warmup):
+    """HIP events around every launch, on the stream the launches go to."""
     import torch
     for _ in range(warmup):
         runner.step()
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(steps)]
+    n_bufs = runner.stops.shape[0]
     t0 = time.perf_counter()
-    for e0, e1 in evs:
+    for i, (e0, e1) in enumerate(evs):
         e0.record()
-        runner.step()
+        runner.step(i % n_bufs)
         e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    runner.check(min(steps, n_bufs))
     per = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
-    time_steps.last = {"kernel_ms_p10": per[int(0.1 * (steps - 1))], "kernel_ms_p50": per[(steps - 1) // 2],
-                       "kernel_ms_p90": per[int(0.9 * (steps - 1))]}
-    return wall, sum(per) / steps
+    spread = {"kernel_ms_p10": per[int(0.1 * (steps - 1))], "kernel_ms_p50": per[(steps - 1) // 2],
+              "kernel_ms_p90": per[int(0.9 * (steps - 1))]}
+    return wall, sum(per) / steps, spread
 
 
-def cpu_baseline(wl, eligible_tokens, tau, phi, patience, budget_s):
-    """The oracle (fp64 C, OpenMP over the (sequence, KV head) groups) on the
-    same workload, repeated whole until the time budget is used (at least
-    once): a bounded sample of steps."""
+def measure(wl, tau, phi, pat, steps, warmup, copies, chunk_blocks=0, no_detector=False,
+            keep_out=False):
+    """One mode of one workload: kernel time, rates, skipped share."""
+    import torch
+    run = Runner(wl, copies, tau, phi, pat, chunk_blocks, no_detector, n_stop_bufs=steps)
+    print(f"[bench] {wl.spec.name}: tau={tau} phi={phi} p={pat} steps={steps}"
+          f"{' no_detector' if no_detector else ''}", file=sys.stderr, flush=True)
+    wall, kern_ms, spread = time_steps(run, steps, warmup)
+    alg, read_tokens, blocks = algorithmic_bytes(wl, run.stop)
+    total_blocks = sum(map(sum, wl.traversal_lengths()))
+    eligible = wl.kv_bytes_in_traversal() // (2 * wl.spec.head_dim * 2)
+    res = {
+        "ms_per_step": wall / steps * 1e3,
+        "kernel_ms": kern_ms,
+        **spread,
+        "effective_tokens_heads_per_s": eligible / (wall / steps),
+        "read_tokens_heads_per_s": read_tokens / (wall / steps),
+        "hbm_gbps_on_bytes_read": alg / (kern_ms * 1e-3) / 1e9,
+        "skipped_pct": 100.0 * (1 - blocks / total_blocks),
+        "blocks_read": blocks, "blocks_total": total_blocks,
+        "alg_bytes_per_launch": alg,
+    }
+    out = run.out.clone() if keep_out else None
+    del run
+    torch.cuda.empty_cache()
+    return res, out
+
+
+def distance_from_full(out_on, out_full):
+    """Relative L2 distance per query head of the output from full attention
+    (termination off): mean, p99, max."""
+    import torch
+    num = torch.linalg.vector_norm((out_on - out_full).double(), dim=-1).flatten()
+    den = torch.linalg.vector_norm(out_full.double(), dim=-1).flatten()
+    rel = torch.where(den > 0, num / den.clamp_min(1e-300), num).cpu().numpy()
+    import numpy as np
+    return {"rel_l2_mean": float(rel.mean()), "rel_l2_p99": float(np.quantile(rel, 0.99)),
+            "rel_l2_max": float(rel.max()), "heads": int(rel.size)}
+
+
+def read_ceiling():
+    """The HBM read rate a plain read-only streaming kernel reaches in this
+    process (16 KiB pieces, 64 KiB in flight per workgroup): 4 GiB read
+    sequentially, and the same pieces in a random order (pages of a pool,
+    as the decode kernel reads them).  Median of 10 launches each."""
+    import ctypes
+    import torch
+    from paper_2606_00024_amd import build
+    lib = ctypes.CDLL(build.BENCH_LIB)
+    lib.art_bench_read.restype = ctypes.c_int
+    lib.art_bench_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    piece = int(lib.art_bench_piece_bytes())
+    nbytes = 4 << 30
+    n = nbytes // piece
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    perm = torch.randperm(n, generator=torch.Generator().manual_seed(1)).to(torch.int32).to("cuda:0")
+    props = torch.cuda.get_device_properties(0)
+    grid = props.multi_processor_count * 8
+    sink = torch.empty(grid * 256, dtype=torch.int32, device="cuda:0")
+    stream = torch.cuda.current_stream().cuda_stream
+    out = {"bytes": nbytes, "piece_bytes": piece, "workgroups": grid}
+    for name, lst in (("sequential", None), ("random_pieces", perm)):
+        def call():
+            rc = lib.art_bench_read(int(buf.data_ptr()), n, 0 if lst is None else int(lst.data_ptr()),
+                                    grid, int(sink.data_ptr()), stream)
+            if rc != 0:
+                raise RuntimeError(f"art_bench_read: hip error {rc}")
+        call()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            call()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        out[f"{name}_gbps"] = nbytes / (sorted(ts)[len(ts) // 2] * 1e-3) / 1e9
+    del buf, perm, sink
+    torch.cuda.empty_cache()
+    out["gbps"] = max(out["sequential_gbps"], out["random_pieces_gbps"])
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, tau, phi, pat):
+    """The oracle (fp64 C, OpenMP over the (sequence, KV head) groups), as it
+    stands, on bounded samples of the same workload: every group with all
+    threads, and the first two groups with one thread; termination on (the
+    bench thresholds) and off; each the median of three runs.  Rates are KV
+    tokens*heads of the traversal set of the sampled groups per second."""
+    import numpy as np
     import oracle
     s = wl.spec
     host = dict(q=wl.q.cpu(), k=wl.k_cache.cpu(), v=wl.v_cache.cpu(), pt=wl.page_table.cpu(),
                 sl=wl.seq_lens.cpu(),
                 bl=None if wl.block_list is None else wl.block_list.cpu(),
                 bll=None if wl.block_list_len is None else wl.block_list_len.cpu())
+    lens = np.asarray(wl.traversal_lengths())
+    Bk = s.block_size
+    seq = host["sl"].numpy()
+
+    def tokens_of(mask):
+        # tokens in the traversal sets of the masked groups
+        tot = 0
+        for b in range(s.batch):
+            for h in range(s.num_kv_heads):
+                if mask[b, h]:
+                    if host["bl"] is None:
+                        tot += int(seq[b])
+                    else:
+                        ids = host["bl"][b, h, : int(lens[b, h])].numpy()
+                        tot += int(sum(min(Bk, int(seq[b]) - int(i) * Bk) for i in ids))
+        return tot
+
+    all_mask = np.ones((s.batch, s.num_kv_heads), dtype=np.uint8)
+    two = np.zeros_like(all_mask)
+    two.reshape(-1)[:2] = 1
     threads = oracle.max_threads()
-    reps, elapsed = 0, 0.0
-    while reps == 0 or elapsed < budget_s:
-        t = time.perf_counter()
-        oracle.decode(host["q"], host["k"], host["v"], host["pt"], host["sl"],
-                      block_size=s.block_size, scale=s.softmax_scale, tau=tau, phi=phi,
-                      patience=patience, dense_order=s.dense_order, block_list=host["bl"],
-                      block_list_len=host["bll"], num_threads=threads)
-        elapsed += time.perf_counter() - t
-        reps += 1
-    return {"value": eligible_tokens * reps / elapsed, "unit": "KV tokens·heads/s",
-            "cores": threads, "kind": "oracle",
-            "sample": f"{reps} whole step(s) of the same workload (all {s.batch * s.num_kv_heads} "
-                      f"groups, same thresholds) in {elapsed:.1f}s, {threads} OpenMP threads"}
+    res = {"unit": "KV tokens·heads/s", "kind": "oracle", "cpu_model": cpu_model(),
+           "nproc": os.cpu_count(), "threads_all": threads}
+    for label, mask, nt in (("all", all_mask, threads), ("one_thread", two, 1)):
+        for mode, t in (("on", tau), ("off", 0.0)):
+            times = []
+            for _ in range(3):
+                t0 = time.perf_counter()
+                oracle.decode(host["q"], host["k"], host["v"], host["pt"], host["sl"],
+                              block_size=Bk, scale=s.softmax_scale, tau=t, phi=phi, patience=pat,
+                              dense_order=s.dense_order, block_list=host["bl"],
+                              block_list_len=host["bll"], group_mask=mask, num_threads=nt)
+                times.append(time.perf_counter() - t0)
+            med = sorted(times)[1]
+            res[f"{label}_{mode}"] = {"seconds_median": med, "tokens_heads": tokens_of(mask),
+                                      "value": tokens_of(mask) / med, "threads": nt,
+                                      "groups": int(mask.sum())}
+    res["value"] = res["all_on"]["value"]
+    res["cores"] = threads
+    res["sample"] = (f"whole step (all {s.batch * s.num_kv_heads} groups) with {threads} OpenMP "
+                     f"threads and the first 2 groups with 1 thread, termination on "
+                     f"(tau={tau}, phi={phi}) and off, median of 3 runs each; "
+                     f"value = all groups, termination on")
+    return res
 
 
 def list_producer_leg(args):
@@ -258,6 +437,19 @@ def list_producer_leg(args):
     print(json.dumps(out), flush=True)
 
 
+def workload_config(spec, wl, W, tau, phi, pat, copies):
+    lens = W.resolve_seq_lens(spec)
+    return {"workload": spec.name, "batch": spec.batch, "q_heads": spec.num_q_heads,
+            "kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim,
+            "seq_lens": (list(spec.seq_lens) if spec.seq_lens[0] == "uniform"
+                         else sorted(set(lens))),
+            "tokens_total": int(sum(lens)),
+            "block_size": spec.block_size, "page_size": spec.page_size,
+            "traversal": "block_list" if wl.block_list is not None else "recent_first",
+            "tau": tau, "phi": phi, "patience": pat, "accumulate": "fp32",
+            "kv_copies_rotated": copies, "seed": spec.seed}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -284,72 +476,37 @@ def main():
         return
 
     spec = W.WORKLOADS[args.workload]
-    tau = spec.tau if args.tau is None else args.tau
-    phi = spec.phi if args.phi is None else args.phi
-    pat = spec.patience if args.patience is None else args.patience
+    tau, phi, pat = thresholds(spec, args)
     print(f"[bench] generating {args.workload}", file=sys.stderr, flush=True)
     wl = W.make_workload(spec, device="cuda:0")
     torch.cuda.synchronize()
-    # tokens*heads in the traversal set (the whole cache for the dense order)
-    eligible_tokens = wl.kv_bytes_in_traversal() // (2 * spec.head_dim * 2)
+    copies = args.copies or default_copies(wl)
+    ceiling = None if (args.no_extra or args.only_headline) else read_ceiling()
 
-    def measure(t, f, p, steps, warmup):
-        run = Runner(wl, args.copies, t, f, p, args.chunk_blocks)
-        print(f"[bench] timing tau={t} phi={f} p={p} steps={steps}", file=sys.stderr, flush=True)
-        wall, kern_ms = time_steps(run, steps, warmup)
-        spread = dict(time_steps.last)
-        alg, read_tokens, blocks = algorithmic_bytes(wl, run.stop)
-        total_blocks = sum(map(sum, wl.traversal_lengths()))
-        ms = wall / steps * 1e3
-        res = {
-            "ms_per_step": ms,
-            "kernel_ms": kern_ms,
-            **spread,
-            "effective_tokens_heads_per_s": eligible_tokens / (wall / steps),
-            "read_tokens_heads_per_s": read_tokens / (wall / steps),
-            "hbm_gbps_on_bytes_read": alg / (kern_ms * 1e-3) / 1e9,
-            "skipped_pct": 100.0 * (1 - blocks / total_blocks),
-            "blocks_read": blocks, "blocks_total": total_blocks,
-            "alg_bytes_per_launch": alg,
-        }
-        del run
-        torch.cuda.empty_cache()
-        return res
+    on, out_on = measure(wl, tau, phi, pat, args.steps, args.warmup, copies, args.chunk_blocks,
+                         args.no_detector, keep_out=True)
+    if args.only_headline:
+        print(json.dumps({"workload": spec.name, "tau": tau, "phi": phi, "patience": pat,
+                          "no_detector": args.no_detector, **on}), flush=True)
+        return
+    off = None
+    out_full = None
+    if not args.no_off:
+        off, out_full = measure(wl, 0.0, phi, pat, max(10, args.steps // 2),
+                                max(5, args.warmup // 2), copies, args.chunk_blocks, keep_out=True)
+    defaults = (tau, phi, pat) == thresholds(spec) and args.chunk_blocks == 0 \
+        and not args.no_detector
 
-    # a measured ceiling beside the published one: a plain device copy of
-    # 1 GiB (read plus written bytes over its HIP-event time, median of 10)
-    def copy_rate_gbps():
-        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(10):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            dst.copy_(src)
-            e1.record()
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1))
-        del src, dst
-        torch.cuda.empty_cache()
-        return 2 * (1 << 30) / (sorted(ts)[len(ts) // 2] * 1e-3) / 1e9
-
-    copy_gbps = copy_rate_gbps()
-    on = measure(tau, phi, pat, args.steps, args.warmup)
-    off = None if args.no_off else measure(0.0, phi, pat, max(5, args.steps // 2), max(2, args.warmup // 2))
-    cpu = None if args.no_cpu else cpu_baseline(wl, eligible_tokens, tau, phi, pat, args.cpu_seconds)
-
-    defaults = (tau, phi, pat) == (spec.tau, spec.phi, spec.patience) and args.chunk_blocks == 0
-
-    def roofline(r, mode):
+    def roofline(r, key):
         ach = r["hbm_gbps_on_bytes_read"]
-        traffic = counted_traffic(args.workload, mode) if defaults else None
+        traffic = counted_traffic(key) if defaults else None
         out = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                "frac": ach / HBM_PEAK_GBPS, "traffic": traffic,
                "kernel": f"art_decode_kernel<{spec.group_size}>", "kernel_ms": r["kernel_ms"],
-               "alg_bytes_per_launch": r["alg_bytes_per_launch"],
-               "measured_copy_gbps": copy_gbps, "frac_of_measured_copy": ach / copy_gbps}
+               "alg_bytes_per_launch": r["alg_bytes_per_launch"]}
+        if ceiling is not None:
+            out["measured_read_gbps"] = ceiling["gbps"]
+            out["frac_of_measured_read"] = ach / ceiling["gbps"]
         if traffic is not None:
             # the rate at which the counted bytes (reads past each stop
             # included) move: how busy HBM is, as opposed to how much of
@@ -357,6 +514,51 @@ def main():
             out["traffic_gbps"] = traffic / (r["kernel_ms"] * 1e-3) / 1e9
             out["traffic_frac"] = out["traffic_gbps"] / HBM_PEAK_GBPS
         return out
+
+    quality = None if out_full is None else distance_from_full(out_on, out_full)
+
+    sweep = None
+    if not args.no_extra and spec.name == HEADLINE and out_full is not None:
+        sweep = []
+        for t, f in W.RAGGED_SWEEP:
+            r, o = measure(wl, t, f, pat, 30, 10, copies, keep_out=True)
+            sweep.append({"tau": t, "phi": f, "kernel_ms": r["kernel_ms"],
+                          "skipped_pct": r["skipped_pct"],
+                          "hbm_gbps_on_bytes_read": r["hbm_gbps_on_bytes_read"],
+                          "frac": r["hbm_gbps_on_bytes_read"] / HBM_PEAK_GBPS,
+                          "effective_tokens_heads_per_s": r["effective_tokens_heads_per_s"],
+                          **distance_from_full(o, out_full)})
+            del o
+    cpu = None if args.no_cpu else cpu_baseline(wl, tau, phi, pat)
+    cfg = workload_config(spec, wl, W, tau, phi, pat, copies)
+    del wl, out_on, out_full
+    torch.cuda.empty_cache()
+
+    others = None
+    if not args.no_extra:
+        others = {}
+        for name in ("llama3_8b_32k", "sparse25_128k", "long_512k", "tiny_4k"):
+            if name == spec.name:
+                continue
+            ospec = W.WORKLOADS[name]
+            print(f"[bench] generating {name}", file=sys.stderr, flush=True)
+            owl = W.make_workload(ospec, device="cuda:0")
+            ot, of, op = thresholds(ospec)
+            oc = default_copies(owl)
+            r_on, _ = measure(owl, ot, of, op, 40, 10, oc)
+            r_off, _ = measure(owl, 0.0, of, op, 40, 10, oc)
+            entry = {"config": workload_config(ospec, owl, W, ot, of, op, oc)}
+            for mode, r in (("on", r_on), ("off", r_off)):
+                entry[mode] = {k: r[k] for k in ("kernel_ms", "kernel_ms_p50", "skipped_pct",
+                                                 "hbm_gbps_on_bytes_read",
+                                                 "effective_tokens_heads_per_s",
+                                                 "alg_bytes_per_launch")}
+                entry[mode]["frac"] = r["hbm_gbps_on_bytes_read"] / HBM_PEAK_GBPS
+                if ceiling is not None:
+                    entry[mode]["frac_of_measured_read"] = r["hbm_gbps_on_bytes_read"] / ceiling["gbps"]
+            others[name] = entry
+            del owl
+            torch.cuda.empty_cache()
 
     line = {
         "metric": "decode-attn KV tokens·heads/s; achieved HBM GB/s on bytes read; % KV blocks skipped",
@@ -367,22 +569,20 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": args.workload, "batch": spec.batch, "q_heads": spec.num_q_heads,
-                   "kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim,
-                   "seq_lens": sorted(set(W.resolve_seq_lens(spec)))[:1] if spec.seq_lens[0] != "uniform" else list(spec.seq_lens),
-                   "block_size": spec.block_size, "page_size": spec.page_size,
-                   "traversal": "block_list" if wl.block_list is not None else "recent_first",
-                   "tau": tau, "phi": phi, "patience": pat, "accumulate": "fp32",
-                   "kv_copies_rotated": args.copies},
+        "config": cfg,
         "hbm_gbps_on_bytes_read": on["hbm_gbps_on_bytes_read"],
         "skipped_pct": on["skipped_pct"],
         "read_tokens_heads_per_s": on["read_tokens_heads_per_s"],
         "kernel_ms": on["kernel_ms"],
         "kernel_ms_p10": on["kernel_ms_p10"], "kernel_ms_p50": on["kernel_ms_p50"],
         "kernel_ms_p90": on["kernel_ms_p90"],
-        "roofline": roofline(on, "on"),
+        "distance_from_full_attention": quality,
+        "roofline": roofline(on, (spec.name, tau, phi, "on")),
         "cpu_baseline": cpu,
-        "termination_off": None if off is None else dict(off, roofline=roofline(off, "off")),
+        "termination_off": None if off is None else dict(off, roofline=roofline(off, (spec.name, 0.0, phi, "off"))),
+        "read_ceiling": ceiling,
+        "threshold_sweep": sweep,
+        "other_workloads": others,
     }
     print(json.dumps(line), flush=True)
 

@@ -20,6 +20,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libart.so")
+# read-only streaming kernels for the benchmark's measured read ceiling
+BENCH_LIB = os.path.join(HERE, "libart_bench.so")
+BENCH_SOURCES = ["art_read_peak.hip"]
 SOURCES = ["art_kernels.hip", "art_lists.hip", "art_static.hip", "art_api.cpp"]
 ARCH = os.environ.get("ART_OFFLOAD_ARCH", "gfx950")
 
@@ -40,10 +43,17 @@ def flags(extra=()) -> list[str]:
 
 
 def build(verbose: bool = False, extra=()) -> str:
-    """Compile every source and link libart.so (always rebuilds)."""
+    """Compile every source and link libart.so and libart_bench.so (always
+    rebuilds)."""
+    _link(LIB, SOURCES, verbose, extra)
+    _link(BENCH_LIB, BENCH_SOURCES, verbose, extra)
+    return LIB
+
+
+def _link(lib: str, sources, verbose: bool, extra) -> None:
     cc = hipcc()
-    tmp = LIB + ".tmp"
-    cmd = [cc, *flags(extra), "-shared", "-o", tmp] + [os.path.join(CSRC, s) for s in SOURCES]
+    tmp = lib + ".tmp"
+    cmd = [cc, *flags(extra), "-shared", "-o", tmp] + [os.path.join(CSRC, s) for s in sources]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
@@ -53,8 +63,7 @@ def build(verbose: bool = False, extra=()) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{out}")
     if verbose and out.strip():
         print(out)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
 
 
 def resource_usage() -> str:

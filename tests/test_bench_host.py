@@ -62,12 +62,35 @@ def test_list_traversal_counts_the_listed_blocks():
 
 
 def test_counted_traffic_needs_the_counted_sources(monkeypatch):
-    key = ("llama3_8b_32k", "on")
-    good = dict(bench.COUNTED_TRAFFIC)
-    monkeypatch.setattr(bench, "COUNTED_TRAFFIC", dict(good, sources_sha256=bench.sources_digest()))
-    assert bench.counted_traffic(*key) == good["bytes"][key]
-    monkeypatch.setattr(bench, "COUNTED_TRAFFIC", dict(good, sources_sha256="0" * 64))
-    assert bench.counted_traffic(*key) is None
+    key = ("qwen3_32b_ragged", 1e-3, 1e-3, "on")
+    table = {"sources_sha256": bench.sources_digest(), "bytes": {key: 123456}}
+    monkeypatch.setattr(bench, "COUNTED_TRAFFIC", table)
+    assert bench.counted_traffic(key) == 123456
+    assert bench.counted_traffic(("qwen3_32b_ragged", 1e-2, 1e-2, "on")) is None
+    monkeypatch.setattr(bench, "COUNTED_TRAFFIC", dict(table, sources_sha256="0" * 64))
+    assert bench.counted_traffic(key) is None
+
+
+def test_headline_is_the_largest_single_gpu_workload():
+    """The default workload is the ragged g = 8 batch (the most KV bytes of
+    the five), at the middle of its swept thresholds."""
+    sizes = {}
+    for name, spec in W.WORKLOADS.items():
+        lens = W.resolve_seq_lens(spec)
+        sizes[name] = sum(lens) * spec.num_kv_heads
+    assert max(sizes, key=sizes.get) == bench.HEADLINE == "qwen3_32b_ragged"
+    assert bench.thresholds(W.WORKLOADS[bench.HEADLINE]) == (1e-3, 1e-3, 5)
+    assert (1e-3, 1e-3) in W.RAGGED_SWEEP
+
+
+def test_distance_from_full_attention():
+    full = torch.zeros((2, 3, 128), dtype=torch.float32)
+    full[..., 0] = 1.0
+    on = full.clone()
+    on[0, 0, 1] = 0.5            # one head moved by half its norm
+    d = bench.distance_from_full(on, full)
+    assert d["heads"] == 6 and d["rel_l2_max"] == 0.5
+    assert abs(d["rel_l2_mean"] - 0.5 / 6) < 1e-12
 
 
 def test_more_than_one_gpu_is_refused_before_any_gpu_work():
