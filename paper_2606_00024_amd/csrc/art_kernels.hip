@@ -346,16 +346,11 @@ __device__ __forceinline__ void fetch_state(__amdgpu_buffer_rsrc_t rs, int rec_o
   }
 }
 
-// An LDS tile record holds sum p v (not normalised); normalise on read.
+// An LDS block record holds the block's normalised output (the loaders
+// normalise it when they write it), its running max and its mass.
 template <int G>
 __device__ __forceinline__ void read_tile(const float* rec, State<G>& s, int lane) {
   read_state<G>(rec, s, lane);
-#pragma unroll
-  for (int k = 0; k < Cfg<G>::HPL; ++k) {
-    const float inv = s.L[k] > 0.f ? fast_rcp(s.L[k]) : 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) s.o[k][e] = __fmul_rn(s.o[k][e], inv);
-  }
 }
 
 // ---- phase 1: one 64-token tile on one wavefront ---------------------------
@@ -391,15 +386,16 @@ __device__ __forceinline__ int clamp_page(const KernelParams& P, int b, int tok)
 //     each half tile is written row-major and read back with
 //     ds_read_b64_tr_b16.  P is split into three bf16 parts (hi + mid + lo
 //     carries 24 significant bits), so P.V keeps fp32 precision.
-// The record written to LDS holds sum_j p_hj v_j [G][128], m_h [G] (base 2),
-// l_h [G].  pg[n] is the (uniform) physical page of 16-token group n.
+// The record written to LDS holds the normalised block output
+// sum_j p_hj v_j / l_h [G][128], m_h [G] (base 2) and l_h [G].  pg[n] is the
+// (uniform) physical page of 16-token group n.
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 constexpr int kVPitch = 144;                  // u16 per row of the V staging buffer (288 B)
 constexpr int kVBufU16 = 32 * kVPitch;        // one half tile: 32 rows
 
 // The first tile of a block writes the block record; each later tile of
 // the block (accumulate) is folded into it: both parts rescaled to the
-// larger running max, in tile order.
+// larger running max and the combined mass, in tile order.
 template <int G>
 __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, const int (&pg)[4],
                              const bf16x8 (&qa)[4], uint16_t* __restrict__ vbuf,
@@ -543,30 +539,38 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
     }
     wave_lds_sync();  // the reads of this half complete before the next half is written
   }
-  // acc[d][r]: head 4g + r, dim 16d + lo
+  // acc[d][r]: head 4g + r, dim 16d + lo.  Row 0 of the lanes (g = 0) holds
+  // (m, l) of head lo; it leaves the factors that normalise (or fold) the
+  // tile's sums in the staging buffer, which the P.V loop no longer reads.
+  float* scale = reinterpret_cast<float*>(vbuf);
   if (!accumulate) {
+    if (g == 0 && lo < G) scale[lo] = ls > 0.f ? fast_rcp(ls) : 0.f;
+    wave_lds_sync();
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int h = 4 * g + r;
       if (h < G) {
+        const float inv = scale[h];
 #pragma unroll
-        for (int d = 0; d < 8; ++d) rec[h * kD + 16 * d + lo] = acc[d][r];
+        for (int d = 0; d < 8; ++d) rec[h * kD + 16 * d + lo] = __fmul_rn(acc[d][r], inv);
       }
     }
+    wave_lds_sync();  // the factors are read before the buffer is reused
     return;
   }
-  // fold into the block record: the lanes of row 0 combine (m, l) of head lo
-  // and leave both scale factors in the (now unused) staging buffer
-  float* scale = reinterpret_cast<float*>(vbuf);
+  // fold into the block record: o = (o_rec L_rec so + sum_tile sn) / L_new
   if (g == 0 && lo < G) {
     const float mo = rec[G * kD + lo], lo_sum = rec[G * kD + G + lo];
     const float mn = fmaxf(mo, mx);
     const float so = mo == kNegInf ? 0.f : fast_exp2(mo - mn);
     const float sn = mx == kNegInf ? 0.f : fast_exp2(mx - mn);
+    const float a = __fmul_rn(lo_sum, so);
+    const float Ln = __fadd_rn(a, __fmul_rn(ls, sn));
+    const float inv = Ln > 0.f ? fast_rcp(Ln) : 0.f;
     rec[G * kD + lo] = mn;
-    rec[G * kD + G + lo] = lo_sum * so + ls * sn;
-    scale[lo] = so;
-    scale[G + lo] = sn;
+    rec[G * kD + G + lo] = Ln;
+    scale[lo] = __fmul_rn(a, inv);
+    scale[G + lo] = __fmul_rn(sn, inv);
   }
   wave_lds_sync();
 #pragma unroll
@@ -577,7 +581,7 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
 #pragma unroll
       for (int d = 0; d < 8; ++d) {
         float* x = rec + h * kD + 16 * d + lo;
-        *x = *x * so + acc[d][r] * sn;
+        *x = __fadd_rn(__fmul_rn(*x, so), __fmul_rn(acc[d][r], sn));
       }
     }
   }
@@ -945,6 +949,9 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   const int rec_agg = k * 2 * P.record_floats;          // float offsets in the group's area
   const int rec_inc = rec_agg + P.record_floats;
 
+  // the predecessor's flag, read now so that the round trip overlaps the
+  // aggregate fold
+  const uint64_t prev_flag = k > 0 ? ld_relaxed(P.flags + (int64_t)gidx * P.max_chunks + (k - 1)) : 0ull;
   // chunk aggregate: w0 (+) (w1 (+) w2) over the loaders' partials, or a
   // left fold over the blocks when the partials did not fit in LDS
   State<G> agg;
@@ -976,7 +983,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   int j;
   if (k == 0) {
     j = -1;
-  } else if (flag_state(ld_relaxed(P.flags + (int64_t)gidx * P.max_chunks + (k - 1)), P.epoch) >= kInclusive) {
+  } else if (flag_state(prev_flag, P.epoch) >= kInclusive) {
     j = k - 1;
   } else {
     publish_state<G>(rs, rec_agg, agg, lane);
@@ -1022,16 +1029,18 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
 
   // Replay the chunk's blocks from the prefix with the stability test.
   // Blocks go in batches of NB: the merges run in order (each needs the
-  // state after the previous block) and leave per-lane partial sums; the
-  // row reductions of the whole batch then run together.
+  // state after the previous block) and leave per-lane partial sums of
+  // |d|^2 and o(t-1).d per head; the row reductions of the whole batch then
+  // run together, and |o(t)|^2 follows as |o(t-1)|^2 + 2 o(t-1).d + |d|^2.
+  // The probe weights (Sec. 3.2, x = P o: 1 on the coordinates the test
+  // looks at, every probe_stride-th of the head dimension, 0 elsewhere)
+  // multiply the partial sums only when the probe is a subsample; this lane
+  // holds coordinates 8*(lane&15) .. +7.
   constexpr int NB = 8 / HPL > 0 ? 8 / HPL : 1;
   uint32_t stable_bits = 0;
+  State<G> s = pre;   // after the replay: the state after the chunk's last block
   {
-    State<G> s = pre;
-    // Probe weights (Sec. 3.2, x = P o): 1 on the coordinates the test looks
-    // at (every probe_stride-th of the head dimension), 0 elsewhere.  This
-    // lane holds coordinates 8*(lane&15) .. +7.  Multiplying by 1 is exact,
-    // so the whole-output test is unchanged bit for bit.
+    const bool full_probe = P.probe_stride == 1;
     float pw[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e)
@@ -1042,16 +1051,16 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     for (int kk = 0; kk < HPL; ++kk) {
       float n0 = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(s.o[kk][e] * pw[e], s.o[kk][e], n0);
+      for (int e = 0; e < 8; ++e) n0 = __builtin_fmaf(full_probe ? s.o[kk][e] : s.o[kk][e] * pw[e], s.o[kk][e], n0);
       n_prev[kk] = row_sum(n0);
     }
     const bool on_acc = P.scale_of_accumulator != 0;
     for (int i0 = 0; i0 < nb; i0 += NB) {
-      float pdd[NB][HPL], pod[NB][HPL], pn1[NB][HPL], pdx[NB][HPL];
+      float pdd[NB][HPL], pod[NB][HPL], pdx[NB][HPL];
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
 #pragma unroll
-        for (int kk = 0; kk < HPL; ++kk) pdd[u][kk] = pod[u][kk] = pn1[u][kk] = pdx[u][kk] = 0.f;
+        for (int kk = 0; kk < HPL; ++kk) pdd[u][kk] = pod[u][kk] = pdx[u][kk] = 0.f;
         const int i = i0 + u;
         if (i < nb) {
           State<G> blkst;
@@ -1067,12 +1076,19 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
           merge<G, true>(s, blkst, d);
 #pragma unroll
           for (int kk = 0; kk < HPL; ++kk) {
-            float dd = 0.f, od = 0.f, n1 = 0.f, dx2 = 0.f;
+            float dd = 0.f, od = 0.f, dx2 = 0.f;
+            if (full_probe) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              dd = __builtin_fmaf(d[kk][e] * pw[e], d[kk][e], dd);
-              od = __builtin_fmaf(old_o[kk][e] * pw[e], d[kk][e], od);
-              n1 = __builtin_fmaf(s.o[kk][e] * pw[e], s.o[kk][e], n1);
+              for (int e = 0; e < 8; ++e) {
+                dd = __builtin_fmaf(d[kk][e], d[kk][e], dd);
+                od = __builtin_fmaf(old_o[kk][e], d[kk][e], od);
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                dd = __builtin_fmaf(d[kk][e] * pw[e], d[kk][e], dd);
+                od = __builtin_fmaf(old_o[kk][e] * pw[e], d[kk][e], od);
+              }
             }
             if (on_acc) {
               // change of the unnormalised accumulator L o, each side in its
@@ -1085,10 +1101,8 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
             }
             pdd[u][kk] = dd;
             pod[u][kk] = od;
-            pn1[u][kk] = n1;
             pdx[u][kk] = dx2;
           }
-          write_state<G>(blocks + i * REC, s, lane);   // o(t) after block i, for the output
         }
       }
       if (incl_pending) raise_inclusive();
@@ -1098,7 +1112,6 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
         for (int kk = 0; kk < HPL; ++kk) {
           pdd[u][kk] = row_sum(pdd[u][kk]);
           pod[u][kk] = row_sum(pod[u][kk]);
-          pn1[u][kk] = row_sum(pn1[u][kk]);
           if (on_acc) pdx[u][kk] = row_sum(pdx[u][kk]);
         }
 #pragma unroll
@@ -1108,7 +1121,8 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
         bool ok = true;
 #pragma unroll
         for (int kk = 0; kk < HPL; ++kk) {
-          const float n0 = n_prev[kk], dd = pdd[u][kk], od = pod[u][kk], n1 = pn1[u][kk];
+          const float n0 = n_prev[kk], dd = pdd[u][kk], od = pod[u][kk];
+          const float n1 = __fadd_rn(__fadd_rn(n0, __fmul_rn(2.f, od)), dd);   // |x(t)|^2
           n_prev[kk] = n1;
           // Eq. (2) on the probe: d_scale = |P d| (or the change of P L o);
           // d_direction = 1 - cos(P o_new, P o_old)
@@ -1167,15 +1181,16 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   if (!stopped_before && y.stopped && sm.fis < 0 && lane == 0)  // the stop lies in this chunk
     announce_stop(P, gidx, k);
   publish_word(P, gidx, k, kStabInclusive, pack_stab(y), lane);
-  wave_lds_sync();  // saved per-block states were written by other lanes
   if (!stopped_before && y.stopped) {
-    // the stop lies in this chunk: write o(t*)
-    State<G> s;
-    read_state<G>(blocks + (y.stop_t - 1 - t0) * REC, s, lane);
-    write_outputs<G>(P, b, kvh, s, y.stop_t, lane);
+    // the stop lies in this chunk: o(t*) again from the prefix, by the same
+    // merges as the replay (the same bits)
+    State<G> o = pre, t;
+    for (int i = 0; i < y.stop_t - t0; ++i) {
+      read_tile<G>(blocks + i * REC, t, lane);
+      merge<G, false>(o, t);
+    }
+    write_outputs<G>(P, b, kvh, o, y.stop_t, lane);
   } else if (!y.stopped && k == n_chunks - 1) {
-    State<G> s;
-    read_state<G>(blocks + (nb - 1) * REC, s, lane);
     write_outputs<G>(P, b, kvh, s, T, lane);
   }
 }
@@ -1245,6 +1260,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
   int qx = blockIdx.x % kQueues;
   uint64_t used_up = 0;
   constexpr uint64_t kAllUsedUp = kQueues >= 64 ? ~0ull : ((1ull << kQueues) - 1ull);
+
   for (int it = 0;; ++it) {
     const int slot = it % n_slots;
     if (lw == 0) {
