@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 6
+#define ART_ABI_VERSION 7
 
 typedef enum {
     ART_OK = 0,
@@ -137,6 +137,15 @@ typedef struct {
     int32_t max_wait_polls;        /* 0 = default (2^22 polls of about a microsecond each);
                                       n > 0: a wait on another workgroup's chunk gives up
                                       after n polls (a watchdog; see art_workspace_status) */
+    int32_t per_head_stop;         /* 0: one stop per (sequence, KV head): a step is stable
+                                      only if it is for every query head of the group;
+                                      1: every query head keeps its own patience counter
+                                      (Eq. 3) and stops on its own; its out and lse are
+                                      those at its own stop, and stop_block is then
+                                      [batch][num_q_heads]: each head's stop (T if it never
+                                      stops).  A group reads blocks until its last head
+                                      has stopped.  Needs a larger workspace
+                                      (art_decode_workspace_bytes) */
 } art_decode_opts;
 
 /* Version of this ABI (ART_ABI_VERSION). */
@@ -173,7 +182,8 @@ art_status art_workspace_init(void* workspace, size_t bytes, hipStream_t stream)
  *                block_list is NULL.  0 gives an empty traversal.
  *   out          [batch][num_q_heads][head_dim], fp32 or bf16 (out_dtype).
  *   lse          fp32 [batch][num_q_heads], natural log; -inf for T = 0.
- *   stop_block   int32 [batch][num_kv_heads]: blocks consumed t* (0..T).
+ *   stop_block   int32 [batch][num_kv_heads]: blocks consumed t* (0..T);
+ *                with per_head_stop, [batch][num_q_heads]: each head's stop.
  *   workspace    see art_decode_workspace_bytes / art_workspace_init.
  * Returns ART_OK once the work is enqueued.  Each call tags the workspace
  * with a fresh value of a host-side counter that is passed as a kernel

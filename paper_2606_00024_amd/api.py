@@ -53,7 +53,8 @@ def make_shape(q, k_cache, v_cache, page_table, *, block_size: int, block_list=N
 def make_opts(*, softmax_scale: float, tau: float, phi: float, patience: int,
               dense_order: int = 0, out_dtype=torch.float32, chunk_blocks: int = 0,
               probe_stride: int = 1, scale_of_accumulator: bool = False,
-              no_detector: bool = False, max_wait_polls: int = 0) -> DecodeOpts:
+              no_detector: bool = False, max_wait_polls: int = 0,
+              per_head_stop: bool = False) -> DecodeOpts:
     od = _lib.OUT_BF16 if out_dtype == torch.bfloat16 else _lib.OUT_F32
     if out_dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_dtype must be float32 or bfloat16")
@@ -62,7 +63,8 @@ def make_opts(*, softmax_scale: float, tau: float, phi: float, patience: int,
                       chunk_blocks=int(chunk_blocks), probe_stride=int(probe_stride),
                       scale_of_accumulator=1 if scale_of_accumulator else 0,
                       no_detector=1 if no_detector else 0,
-                      max_wait_polls=int(max_wait_polls))
+                      max_wait_polls=int(max_wait_polls),
+                      per_head_stop=1 if per_head_stop else 0)
 
 
 def workspace_bytes(shape: DecodeShape, opts: DecodeOpts) -> int:
@@ -97,7 +99,7 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                      list_per_head: bool = True, out_dtype=torch.float32,
                      chunk_blocks: int = 0, probe_stride: int = 1,
                      scale_of_accumulator: bool = False, no_detector: bool = False,
-                     max_wait_polls: int = 0,
+                     max_wait_polls: int = 0, per_head_stop: bool = False,
                      workspace: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      stop_block: Optional[torch.Tensor] = None):
@@ -113,6 +115,9 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     test at all (full attention over the traversal).  ``max_wait_polls``
     n > 0 makes every wait of the kernel give up after n polls (the call then
     reports ART_ERR_DEVICE_TIMEOUT through ``workspace_status``).
+    ``per_head_stop`` gives every query head its own patience counter and stop
+    (out and lse at the head's own stop; stop_block is then [B][Hq], each
+    head's stop).
     """
     _require_cuda(q, "q", torch.bfloat16)
     _require_cuda(k_cache, "k_cache", torch.bfloat16)
@@ -137,14 +142,15 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     opts = make_opts(softmax_scale=softmax_scale, tau=tau, phi=phi, patience=patience,
                      dense_order=dense_order, out_dtype=out_dtype, chunk_blocks=chunk_blocks,
                      probe_stride=probe_stride, scale_of_accumulator=scale_of_accumulator,
-                     no_detector=no_detector, max_wait_polls=max_wait_polls)
+                     no_detector=no_detector, max_wait_polls=max_wait_polls,
+                     per_head_stop=per_head_stop)
     dev = q.device
     if out is None:
         out = torch.empty((B, Hq, D), dtype=out_dtype, device=dev)
     if lse is None:
         lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     if stop_block is None:
-        stop_block = torch.empty((B, Hkv), dtype=torch.int32, device=dev)
+        stop_block = torch.empty((B, Hq if per_head_stop else Hkv), dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
     need = workspace_bytes(shape, opts)
     ws = workspace if workspace is not None else _cached_workspace(need, dev, stream)

@@ -74,7 +74,8 @@ art_status check_shape(const art_decode_shape* s, const art_decode_opts* o) {
         (o->probe_stride & (o->probe_stride - 1)) != 0 ||
         (o->probe_stride > 1 && s->head_dim % o->probe_stride != 0) ||
         (o->scale_of_accumulator != 0 && o->scale_of_accumulator != 1) ||
-        (o->no_detector != 0 && o->no_detector != 1) || o->max_wait_polls < 0)
+        (o->no_detector != 0 && o->no_detector != 1) || o->max_wait_polls < 0 ||
+        (o->per_head_stop != 0 && o->per_head_stop != 1))
         return ART_ERR_INVALID_ARG;
     const int g = s->num_q_heads / s->num_kv_heads;
     if (s->head_dim != art::kHeadDim) return ART_ERR_UNSUPPORTED;
@@ -179,6 +180,8 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     w.stop_off = off;       off = align_up(off + 8 * (size_t)n_groups);
     w.flags_off = off;      off = align_up(off + 8 * (size_t)n_groups * max_chunks);
     w.records_off = off;    off = align_up(off + (size_t)n_groups * max_chunks * 2 * p->record_floats * 4);
+    w.head_off = off;
+    if (o->per_head_stop && !o->no_detector) off = align_up(off + (size_t)n_groups * max_chunks * g * 8 * 4);
     // one group's records are addressed with 32-bit byte offsets
     if ((int64_t)max_chunks * 2 * p->record_floats * 4 > INT32_MAX) return ART_ERR_UNSUPPORTED;
     w.total = off;
@@ -236,6 +239,7 @@ art_status enqueue_decode(const Plan& plan, const art_decode_shape* shape,
     k.probe_stride = opts->probe_stride > 1 ? opts->probe_stride : 1;
     k.scale_of_accumulator = opts->scale_of_accumulator;
     k.no_detector = opts->no_detector;
+    k.per_head = opts->per_head_stop && !opts->no_detector;
     k.dense_order = opts->dense_order;
     k.out_bf16 = opts->out_dtype == ART_OUT_BF16;
     k.tiles_per_block = plan.tiles_per_block;
@@ -273,6 +277,7 @@ art_status enqueue_decode(const Plan& plan, const art_decode_shape* shape,
     k.stop_word = reinterpret_cast<uint64_t*>(ws + plan.ws.stop_off);
     k.flags = reinterpret_cast<uint64_t*>(ws + plan.ws.flags_off);
     k.records = reinterpret_cast<float*>(ws + plan.ws.records_off);
+    k.head_area = reinterpret_cast<int32_t*>(ws + plan.ws.head_off);
     k.epoch = next_epoch();
     k.spin_limit = opts->max_wait_polls > 0 ? (uint32_t)opts->max_wait_polls : kSpinLimit;
     if (k.epoch >= (uint64_t(1) << 40)) return ART_ERR_UNSUPPORTED;

@@ -42,6 +42,7 @@ struct WorkspaceLayout {
     size_t stop_off;         // uint64 [groups] announced stop: epoch << 24 | chunk
     size_t flags_off;        // uint64 [groups][max_chunks]: epoch << 24 | state << 20 | payload
     size_t records_off;      // float [groups][max_chunks][2][record_floats]
+    size_t head_off;         // per-head mode: int32 [groups][max_chunks][g][8]; else 0 bytes
     size_t total;
 };
 
@@ -74,6 +75,7 @@ struct KernelParams {
     int32_t probe_stride;    // the stability test sees coordinates 0, s, 2s, ... (1 = all)
     int32_t scale_of_accumulator;  // 1: d_scale on the unnormalised accumulator L o
     int32_t no_detector;     // 1: no stability test at all (full attention over the traversal)
+    int32_t per_head;        // 1: every query head has its own patience counter and stop
     // plan
     int32_t tiles_per_block, chunk_blocks, max_chunks, t_cap, record_floats;
     int32_t lead_chunks, lead_blocks;  // the first lead_chunks chunks hold lead_blocks blocks
@@ -98,6 +100,7 @@ struct KernelParams {
     uint64_t* stop_word;
     uint64_t* flags;
     float* records;
+    int32_t* head_area;      // per-head mode: [groups][max_chunks][g][8] int32
     uint64_t epoch;          // unique per call; tags every flag it writes
     uint32_t spin_limit;     // polls before a wait gives up
 };

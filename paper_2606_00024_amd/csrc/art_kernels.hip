@@ -778,12 +778,13 @@ __device__ __forceinline__ void publish_word(const KernelParams& P, int gidx, in
 }
 template <int G>
 __device__ void write_outputs(const KernelParams& P, int b, int kvh, const State<G>& s,
-                              int stop, int lane) {
+                              int stop, int lane, uint32_t heads = 0xffffffffu,
+                              bool write_stop = true) {
   const int c = lane & 15, r = lane >> 4;
 #pragma unroll
   for (int k = 0; k < Cfg<G>::HPL; ++k) {
     const int h = r + 4 * k;
-    if (h >= G) continue;
+    if (h >= G || !((heads >> h) & 1u)) continue;
     const int64_t row = (int64_t)b * P.num_q_heads + kvh * G + h;
     if (P.out_bf16) {
       uint32_t w[4];
@@ -801,18 +802,7 @@ __device__ void write_outputs(const KernelParams& P, int b, int kvh, const State
       P.lse[row] = (s.m[k] + __log2f(s.L[k])) * 0.69314718055994531f;
     }
   }
-  if (lane == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = stop;
-}
-
-template <int G>
-__device__ void write_empty(const KernelParams& P, int b, int kvh) {
-  for (int i = threadIdx.x; i < G * kD; i += blockDim.x) {
-    const int64_t idx = ((int64_t)b * P.num_q_heads + kvh * G) * kD + i;
-    if (P.out_bf16) static_cast<uint16_t*>(P.out)[idx] = 0;
-    else static_cast<float*>(P.out)[idx] = 0.f;
-  }
-  if ((int)threadIdx.x < G) P.lse[(int64_t)b * P.num_q_heads + kvh * G + threadIdx.x] = kNegInf;
-  if (threadIdx.x == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = 0;
+  if (write_stop && lane == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = stop;
 }
 
 struct GroupInfo {
@@ -863,7 +853,11 @@ __device__ void write_empty_wave(const KernelParams& P, int b, int kvh, int lane
     else static_cast<float*>(P.out)[idx] = 0.f;
   }
   if (lane < G) P.lse[(int64_t)b * P.num_q_heads + kvh * G + lane] = kNegInf;
-  if (lane == 0) P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = 0;
+  if (P.per_head) {
+    if (lane < G) P.stop_block[(int64_t)b * P.num_q_heads + kvh * G + lane] = 0;
+  } else if (lane == 0) {
+    P.stop_block[(int64_t)b * P.num_kv_heads + kvh] = 0;
+  }
 }
 
 constexpr int kLoaders = kWaves - 1;   // wavefronts 1..3 stream tiles
@@ -936,9 +930,161 @@ __device__ int claim_finish(const KernelParams& P, int x, uint64_t v, int lane) 
   return __builtin_amdgcn_readfirstlane(q);
 }
 
+// ---- per-query-head termination ---------------------------------------------
+// The per-head reading of the test: every query head of a group keeps its
+// own patience counter (Eq. 3) and stops on its own; its out and lse are
+// those at its own stop (stop_block [batch][num_q_heads] holds each head's
+// stop, T for a head that never stops), and the group stops reading blocks
+// once its last head has stopped.  The chunk's summaries
+// and states of the stability monoid are kept per head in the workspace's
+// head area, [chunk][head][8] int32 (lead, trail, len, fis | stopped, run),
+// written by lane h for head h and published by the chunk's flag as in the
+// group reading.  A summary stays valid after the chunk's state is
+// published, so the fold below never meets a changed word.
+__device__ __forceinline__ int32_t* head_area(const KernelParams& P, int gidx, int k, int G) {
+  return P.head_area + ((int64_t)gidx * P.max_chunks + k) * (int64_t)(G * 8);
+}
+
+// The nearest chunk before `me` that published its stability state, such
+// that every chunk between published its summary: j >= -1, or -2 when a
+// stop before `me` has been announced or a wait gave up.
+__device__ int stab_scan(const KernelParams& P, int gidx, int me, int lane) {
+  const uint64_t* flags = P.flags + (int64_t)gidx * P.max_chunks;
+  int hi = me - 1;
+  uint32_t it = 0;
+  while (hi >= 0) {
+    const int idx = hi - lane;
+    const uint32_t st = idx >= 0 ? flag_state(ld_relaxed(flags + idx), P.epoch) : 0u;
+    const uint64_t have_st = __ballot(idx >= 0 && st >= kStabInclusive);
+    const uint64_t have_sum = __ballot(idx < 0 || st >= kStabSummary);
+    const int first = have_st ? __ffsll((unsigned long long)have_st) - 1 : 64;
+    const uint64_t need = first >= 64 ? ~0ull : ((1ull << first) - 1ull);
+    if ((have_sum & need) == need) {
+      if (first < 64) return hi - first;
+      hi -= 64;
+      continue;
+    }
+    if (stop_announced_before(P, gidx, me)) return -2;
+    if (wait_expired(P, ++it)) return -2;
+    __builtin_amdgcn_s_sleep(2);
+  }
+  return -1;
+}
+
+template <int G>
+__device__ void resolve_heads(const KernelParams& P, int gidx, int k, const GroupInfo& gi,
+                              const float* blocks, const State<G>& pre, uint32_t head_bits,
+                              int t0, int nb, int lane) {
+  constexpr int REC = Cfg<G>::REC;
+  const int n_chunks = gi.n_chunks, T = gi.T;
+  const bool mine = lane < G;   // lane h holds head h
+  int32_t* my = head_area(P, gidx, k, G) + lane * 8;
+  StabSummary sm{0, 0, 0, -1};
+  if (mine) {
+    int run = 0, lead = 0, fis = -1;
+    bool leading = true;
+    for (int i = 0; i < nb; ++i) {
+      const bool st = (head_bits >> i) & 1u;
+      run = st ? run + 1 : 0;
+      if (leading) {
+        if (st) ++lead;
+        else leading = false;
+      }
+      if (fis < 0 && run >= P.patience) fis = i;
+    }
+    sm = StabSummary{lead, run, nb, fis};
+    st_coh_i32(my + 0, lead);
+    st_coh_i32(my + 1, run);
+    st_coh_i32(my + 2, nb);
+    st_coh_i32(my + 3, fis);
+  }
+  stores_complete();
+  publish_word(P, gidx, k, kStabSummary, 0u, lane);
+  // every head reaches its patience inside this chunk: the group's stop lies
+  // here or before, whatever the chunks before hold
+  const bool all_fis = __all(!mine || sm.fis >= 0);
+  if (all_fis && lane == 0) announce_stop(P, gidx, k);
+  // no head can stop in a chunk whose first block is unstable for it and
+  // whose own runs stay short (the last chunk still writes what is left)
+  if (__all(!mine || (sm.lead == 0 && sm.fis < 0)) && k != n_chunks - 1) return;
+
+  // entering state per head: the nearest published state, then the
+  // summaries after it, folded in order (four chunks' words in flight)
+  const int j = stab_scan(P, gidx, k, lane);
+  if (j == -2) return;
+  StabState x{0, 0, 0, 0};
+  if (mine && j >= 0) {
+    const int32_t* w = head_area(P, gidx, j, G) + lane * 8;
+    x.stopped = ld_coh_i32(w + 4);
+    x.run = ld_coh_i32(w + 5);
+  }
+  for (int i0 = j + 1; i0 < k; i0 += 4) {
+    const int n = min(4, k - i0);
+    int32_t v[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (mine && u < n) {
+        const int32_t* w = head_area(P, gidx, i0 + u, G) + lane * 8;
+#pragma unroll
+        for (int f = 0; f < 4; ++f) v[u][f] = ld_coh_i32(w + f);
+      }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (mine && u < n)
+        x = stab_fold(x, StabSummary{v[u][0], v[u][1], v[u][2], v[u][3]}, chunk_start(P, i0 + u), P.patience);
+  }
+  const StabState y = mine ? stab_fold(x, sm, t0, P.patience) : x;
+  if (mine) {
+    st_coh_i32(my + 4, y.stopped);
+    st_coh_i32(my + 5, y.run);
+  }
+  stores_complete();
+  const bool all_before = __all(!mine || x.stopped);
+  const bool all_after = __all(!mine || y.stopped);
+  if (!all_before && all_after && !all_fis && lane == 0) announce_stop(P, gidx, k);
+  publish_word(P, gidx, k, kStabInclusive, 0u, lane);
+  if (all_before) return;   // every head stopped before this chunk
+
+  // heads whose stop lies in this chunk: o(t_h) again from the prefix, by
+  // the same merges as the replay
+  const int rel = (mine && !x.stopped && y.stopped) ? y.stop_t - t0 - 1 : -1;
+  int rel_h[G];
+  int last_rel = -1;
+  uint32_t never = 0;
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    rel_h[h] = __builtin_amdgcn_readlane(rel, h);
+    last_rel = max(last_rel, rel_h[h]);
+    if (!__builtin_amdgcn_readlane((int)y.stopped, h)) never |= 1u << h;
+  }
+  int32_t* head_stop = P.stop_block + (int64_t)gi.b * P.num_q_heads + gi.kvh * G;
+  if (rel >= 0) head_stop[lane] = y.stop_t;
+  // one pass of the replay's merges from the prefix: each head stopping
+  // here is written at its block; in the group's last chunk, heads that
+  // never stopped get the state after the last block (the whole traversal)
+  const bool finish = !all_after && k == n_chunks - 1;
+  const int upto = finish ? nb - 1 : last_rel;
+  if (upto >= 0) {
+    State<G> o = pre, t;
+    for (int i = 0; i <= upto; ++i) {
+      read_tile<G>(blocks + i * REC, t, lane);
+      merge<G, false>(o, t);
+      uint32_t here = 0;
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+        if (rel_h[h] == i) here |= 1u << h;
+      if (here) write_outputs<G>(P, gi.b, gi.kvh, o, 0, lane, here, false);
+    }
+    if (finish) {
+      write_outputs<G>(P, gi.b, gi.kvh, o, T, lane, never, false);
+      if (mine && ((never >> lane) & 1u)) head_stop[lane] = T;
+    }
+  }
+}
+
 // Phase 2 for one chunk (resolver wavefront).  `blocks` holds the chunk's
 // block records, `aggbuf` the loaders' partial aggregates (nagg of them).
-template <int G>
+template <int G, bool PH>
 __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const GroupInfo& gi,
                               float* blocks, const float* aggbuf, int nagg, int lane) {
   constexpr int REC = Cfg<G>::REC;
@@ -1038,6 +1184,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   // holds coordinates 8*(lane&15) .. +7.
   constexpr int NB = 8 / HPL > 0 ? 8 / HPL : 1;
   uint32_t stable_bits = 0;
+  uint32_t head_bits = 0;   // per-head mode: lane h < G, head h's stable blocks
   State<G> s = pre;   // after the replay: the state after the chunk's last block
   {
     const bool full_probe = P.probe_stride == 1;
@@ -1138,6 +1285,12 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
           }
           const bool st = (n0 > 0.f) && (n1 > 0.f) && (d_scale < P.tau) && (d_dir < P.phi);
           if (slot_valid<G>(lane, kk) && !st) ok = false;
+          if (PH) {
+            // lane h < G collects head h's verdicts: head h sits in slot
+            // h / 4 of the lanes of row h % 4
+            const uint64_t bal = __ballot(st);
+            if (lane < G && (lane >> 2) == kk) head_bits |= (uint32_t)((bal >> (16 * (lane & 3))) & 1ull) << i;
+          }
         }
         const bool all_ok = __all(ok);
         stable_bits |= (all_ok ? 1u : 0u) << i;
@@ -1145,6 +1298,10 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     }
   }
 
+  if constexpr (PH) {
+    resolve_heads<G>(P, gidx, k, gi, blocks, pre, head_bits, t0, nb, lane);
+    return;
+  }
   // stability summary of this chunk (entering run 0)
   StabSummary sm;
   {
@@ -1201,7 +1358,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
 // turn; wavefront 0 resolves earlier chunks meanwhile.  A chunk is claimed
 // only once a buffer is free, and every wait targets a chunk claimed
 // earlier, so the launch always makes progress.
-template <int G>
+template <int G, bool PH>
 __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
   // the dynamic buffers must start 16-byte aligned (128-bit LDS accesses):
   // the static block below is a multiple of 16 bytes
@@ -1245,7 +1402,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         float* base = smem + slot * slot_floats;
         const GroupInfo gi = group_info_raw(P, gidx, lds_ld(&s_meta[slot][kMetaLen]),
                                             lds_ld(&s_meta[slot][kMetaListLen]));
-        resolve_chunk<G>(P, gidx, k, gi, base, base + CT * REC, nagg, lane);
+        resolve_chunk<G, PH>(P, gidx, k, gi, base, base + CT * REC, nagg, lane);
       }
       wave_lds_sync();
       if (lane == 0) lds_st(&s_meta[slot][kMetaState], kSlotFree);
@@ -1416,7 +1573,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n_words) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_words; i += stride) p[i] = 0u;
 }
 
-template <int G>
+template <int G, bool PH>
 int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
   const int64_t work = (int64_t)plan.n_groups * plan.max_chunks;
   if (work <= 0) return (int)hipSuccess;
@@ -1424,7 +1581,7 @@ int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e == hipSuccess)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, art_decode_kernel<G>, kThreads, plan.lds_bytes);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, art_decode_kernel<G, PH>, kThreads, plan.lds_bytes);
   if (e != hipSuccess) return (int)e;
   if (per_cu < 1) per_cu = 1;
   // As many workgroups as the chip holds, but at most 32 per group (and
@@ -1432,7 +1589,8 @@ int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
   // nothing but reads past their stops.
   const int64_t per_groups = max((int64_t)cus, (int64_t)32 * plan.n_groups);
   const int64_t grid = min(work, min((int64_t)cus * per_cu, per_groups));
-  hipLaunchKernelGGL(art_decode_kernel<G>, dim3((unsigned)grid), dim3(kThreads),
+  auto kernel = art_decode_kernel<G, PH>;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kThreads),
                      plan.lds_bytes, stream, params);
   return (int)hipGetLastError();
 }
@@ -1441,11 +1599,11 @@ int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
 
 int launch_decode(const Plan& plan, const KernelParams& params, hipStream_t stream) {
   switch (plan.group) {
-    case 1: return launch_g<1>(plan, params, stream);
-    case 2: return launch_g<2>(plan, params, stream);
-    case 4: return launch_g<4>(plan, params, stream);
-    case 8: return launch_g<8>(plan, params, stream);
-    case 16: return launch_g<16>(plan, params, stream);
+    case 1: return params.per_head ? launch_g<1, true>(plan, params, stream) : launch_g<1, false>(plan, params, stream);
+    case 2: return params.per_head ? launch_g<2, true>(plan, params, stream) : launch_g<2, false>(plan, params, stream);
+    case 4: return params.per_head ? launch_g<4, true>(plan, params, stream) : launch_g<4, false>(plan, params, stream);
+    case 8: return params.per_head ? launch_g<8, true>(plan, params, stream) : launch_g<8, false>(plan, params, stream);
+    case 16: return params.per_head ? launch_g<16, true>(plan, params, stream) : launch_g<16, false>(plan, params, stream);
     default: return (int)hipErrorInvalidValue;
   }
 }

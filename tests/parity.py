@@ -224,3 +224,64 @@ def compare_workload(wl, gpu, *, tau, phi, patience, dense_order=None, report=No
     if name is not None:
         record(name, rep)
     return rep
+
+
+def compare_per_head(wl, gpu, *, tau, phi, patience, host=None, name=None, probe_stride=1,
+                     report=None) -> Report:
+    """Per-query-head termination (stop_block [B][Hq]: each head's stop):
+    every head's stop bit-exact against the oracle's per-head stop, except a
+    near-tie of that head alone (its stop reachable by the patience replay
+    over its own trajectory with the in-band steps free); out and lse per
+    head against the oracle at the head's stop (re-run with that head forced
+    to stop where the GPU's did when they differ)."""
+    rep = report or Report()
+    s = wl.spec
+    g = s.group_size
+    src = host if host is not None else wl
+    out, lse, stop = (x.detach().float().cpu().numpy() if x.dtype != torch.int32 else x.cpu().numpy()
+                      for x in gpu)
+    lens = np.asarray(wl.traversal_lengths())
+    kw = dict(probe_stride=probe_stride, per_head_stop=True)
+    ref = oracle.decode_workload(src, tau=tau, phi=phi, patience=patience, **kw)
+    for b in range(s.batch):
+        for h in range(s.num_kv_heads):
+            T = int(lens[b, h])
+            mask = np.zeros((s.batch, s.num_kv_heads), dtype=np.uint8)
+            mask[b, h] = 1
+            trace = None
+            for i in range(g):
+                q = h * g + i
+                rep.groups += 1
+                sg, sr = int(stop[b, q]), int(ref["head_stop"][b, q])
+                o_r, l_r = ref["out"][b, q], ref["lse"][b, q]
+                if sg != sr:
+                    if trace is None:
+                        trace = oracle.decode_workload(src, tau=tau, phi=phi, patience=NO_STOP,
+                                                       group_mask=mask, trace_steps=max(T, 1),
+                                                       probe_stride=probe_stride)["trace"][b, h]
+                    if not excused(trace[:, i:i + 1], T, sg, sr, tau, phi, patience):
+                        rep.failures.append(((b, q), "head stop", sg, sr))
+                        continue
+                    rep.near_ties.append(((b, q), sg, sr))
+                    fs = np.zeros((s.batch, s.num_q_heads), dtype=np.int32)
+                    fs[b, q] = sg
+                    r = oracle.decode_workload(src, tau=tau, phi=phi, patience=patience,
+                                               force_stop=fs, group_mask=mask, **kw)
+                    o_r, l_r = r["out"][b, q], r["lse"][b, q]
+                else:
+                    rep.stop_equal += 1
+                if sr == 0 and sg == 0:
+                    if np.any(out[b, q] != 0) or not np.isneginf(lse[b, q]):
+                        rep.failures.append(((b, q), "empty"))
+                    continue
+                err = float(_rel_l2(out[b, q][None].astype(np.float64), o_r[None])[0])
+                lerr = abs(float(lse[b, q]) - float(l_r))
+                rep.max_rel_l2 = max(rep.max_rel_l2, err)
+                rep.max_lse_err = max(rep.max_lse_err, lerr)
+                if not (err <= OUT_TOL):
+                    rep.failures.append(((b, q), "out", err))
+                if not (lerr <= LSE_TOL):
+                    rep.failures.append(((b, q), "lse", lerr))
+    if name is not None:
+        record(name, rep)
+    return rep

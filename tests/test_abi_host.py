@@ -94,6 +94,7 @@ def test_shape_errors(lib, kw, status):
     dict(softmax_scale=float("inf")), dict(probe_stride=-1), dict(probe_stride=3),
     dict(probe_stride=6), dict(probe_stride=256), dict(scale_of_accumulator=2),
     dict(no_detector=-1), dict(no_detector=2), dict(max_wait_polls=-1),
+    dict(per_head_stop=2), dict(per_head_stop=-1),
 ])
 def test_option_errors(lib, kw):
     n, st = _ws(_shape(), _opts(**kw))
@@ -106,6 +107,16 @@ def test_probe_strides_accepted(lib, stride):
     does not depend on it."""
     n, st = _ws(_shape(), _opts(probe_stride=stride))
     assert st == _lib.OK and n == _ws(_shape(), _opts())[0]
+
+
+def test_per_head_workspace_holds_the_head_records(lib):
+    """Per-head termination adds [groups][chunks][g][8] int32 of per-head
+    stability records; without the detector there is nothing to keep."""
+    a, st = _ws(_shape(), _opts())
+    b, st2 = _ws(_shape(), _opts(per_head_stop=1))
+    c, _ = _ws(_shape(), _opts(per_head_stop=1, no_detector=1))
+    assert st == st2 == _lib.OK
+    assert b > a and c == a
 
 
 def test_workspace_size_depends_on_shape_only(lib):
