@@ -74,49 +74,76 @@ def load() -> ctypes.CDLL:
     """Load the in-tree libart.so; raises if it has not been built."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(
-                f"{LIB_PATH} is missing: build it with `python -m paper_2606_00024_amd.build` "
-                "(there is no fallback implementation)")
-        lib = ctypes.CDLL(LIB_PATH)
-        vp = ctypes.c_void_p
-        i32p = ctypes.POINTER(ctypes.c_int32)
-        lib.art_abi_version.restype = ctypes.c_int32
-        lib.art_abi_version.argtypes = []
-        lib.art_status_str.restype = ctypes.c_char_p
-        lib.art_status_str.argtypes = [ctypes.c_int32]
-        lib.art_decode_workspace_bytes.restype = ctypes.c_size_t
-        lib.art_decode_workspace_bytes.argtypes = [ctypes.POINTER(DecodeShape),
-                                                   ctypes.POINTER(DecodeOpts), i32p]
-        lib.art_workspace_init.restype = ctypes.c_int
-        lib.art_workspace_init.argtypes = [vp, ctypes.c_size_t, vp]
-        lib.art_decode_attention.restype = ctypes.c_int
-        lib.art_decode_attention.argtypes = [
-            ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts),
-            vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
-        lib.art_decode_attention_static.restype = ctypes.c_int
-        lib.art_decode_attention_static.argtypes = [
-            ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts),
-            vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
-        lib.art_validate_inputs.restype = ctypes.c_int
-        lib.art_validate_inputs.argtypes = [
-            ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts), vp, vp, vp, vp, vp,
-            ctypes.POINTER(ctypes.c_int64), i32p]
-        lib.art_workspace_status.restype = ctypes.c_int
-        lib.art_workspace_status.argtypes = [vp, ctypes.c_size_t, vp, i32p]
-        lib.art_block_list_workspace_bytes.restype = ctypes.c_size_t
-        lib.art_block_list_workspace_bytes.argtypes = [ctypes.POINTER(DecodeShape),
-                                                       ctypes.POINTER(ListOpts), i32p]
-        lib.art_build_block_list.restype = ctypes.c_int
-        lib.art_build_block_list.argtypes = [
-            ctypes.POINTER(DecodeShape), ctypes.POINTER(ListOpts), vp, vp, vp, vp, vp, vp, vp,
-            vp, ctypes.c_size_t, vp]
-        got = int(lib.art_abi_version())
-        if got != ABI_VERSION:
-            raise RuntimeError(f"{LIB_PATH} has ABI version {got}, this binding needs "
-                               f"{ABI_VERSION}: rebuild it")
-        _lib = lib
+        _lib = load_variant(LIB_PATH)
     return _lib
+
+
+def load_variant(path: str) -> ctypes.CDLL:
+    """Load a build of the library at `path` (the in-tree libart.so, or a
+    test build of the same sources such as the race-stress build) with the
+    argument types of this binding."""
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with `python -m paper_2606_00024_amd.build` "
+            "(there is no fallback implementation)")
+    lib = ctypes.CDLL(path)
+    vp = ctypes.c_void_p
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.art_abi_version.restype = ctypes.c_int32
+    lib.art_abi_version.argtypes = []
+    lib.art_status_str.restype = ctypes.c_char_p
+    lib.art_status_str.argtypes = [ctypes.c_int32]
+    lib.art_decode_workspace_bytes.restype = ctypes.c_size_t
+    lib.art_decode_workspace_bytes.argtypes = [ctypes.POINTER(DecodeShape),
+                                               ctypes.POINTER(DecodeOpts), i32p]
+    lib.art_workspace_init.restype = ctypes.c_int
+    lib.art_workspace_init.argtypes = [vp, ctypes.c_size_t, vp]
+    lib.art_decode_attention.restype = ctypes.c_int
+    lib.art_decode_attention.argtypes = [
+        ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts),
+        vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.art_decode_attention_static.restype = ctypes.c_int
+    lib.art_decode_attention_static.argtypes = [
+        ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts),
+        vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.art_validate_inputs.restype = ctypes.c_int
+    lib.art_validate_inputs.argtypes = [
+        ctypes.POINTER(DecodeShape), ctypes.POINTER(DecodeOpts), vp, vp, vp, vp, vp,
+        ctypes.POINTER(ctypes.c_int64), i32p]
+    lib.art_workspace_status.restype = ctypes.c_int
+    lib.art_workspace_status.argtypes = [vp, ctypes.c_size_t, vp, i32p]
+    lib.art_block_list_workspace_bytes.restype = ctypes.c_size_t
+    lib.art_block_list_workspace_bytes.argtypes = [ctypes.POINTER(DecodeShape),
+                                                   ctypes.POINTER(ListOpts), i32p]
+    lib.art_build_block_list.restype = ctypes.c_int
+    lib.art_build_block_list.argtypes = [
+        ctypes.POINTER(DecodeShape), ctypes.POINTER(ListOpts), vp, vp, vp, vp, vp, vp, vp,
+        vp, ctypes.c_size_t, vp]
+    got = int(lib.art_abi_version())
+    if got != ABI_VERSION:
+        raise RuntimeError(f"{path} has ABI version {got}, this binding needs "
+                           f"{ABI_VERSION}: rebuild it")
+    return lib
+
+
+class using:
+    """Context manager: calls through this module go to `lib` (a
+    load_variant result) inside the block."""
+
+    def __init__(self, lib):
+        self.lib = lib
+
+    def __enter__(self):
+        global _lib
+        load()
+        self.saved = _lib
+        _lib = self.lib
+        return self.lib
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self.saved
+        return False
 
 
 def status_str(status: int) -> str:

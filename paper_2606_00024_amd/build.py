@@ -23,6 +23,9 @@ LIB = os.path.join(HERE, "libart.so")
 # read-only streaming kernels for the benchmark's measured read ceiling
 BENCH_LIB = os.path.join(HERE, "libart_bench.so")
 BENCH_SOURCES = ["art_read_peak.hip"]
+# the race-stress test build: the same library with seeded delays at every
+# hand-over between workgroups (ART_RACE_STRESS), loaded only by its test
+STRESS_LIB = os.path.join(HERE, "libart_stress.so")
 SOURCES = ["art_kernels.hip", "art_lists.hip", "art_static.hip", "art_api.cpp"]
 ARCH = os.environ.get("ART_OFFLOAD_ARCH", "gfx950")
 
@@ -43,10 +46,11 @@ def flags(extra=()) -> list[str]:
 
 
 def build(verbose: bool = False, extra=()) -> str:
-    """Compile every source and link libart.so and libart_bench.so (always
-    rebuilds)."""
+    """Compile every source and link libart.so, libart_bench.so and the
+    race-stress build libart_stress.so (always rebuilds)."""
     _link(LIB, SOURCES, verbose, extra)
     _link(BENCH_LIB, BENCH_SOURCES, verbose, extra)
+    _link(STRESS_LIB, SOURCES, verbose, (*extra, "-DART_RACE_STRESS"))
     return LIB
 
 

@@ -192,6 +192,27 @@ template <typename Params>
 __device__ __forceinline__ bool launch_failed(const Params& P) {
   return (ld_relaxed(P.error_word) >> 8) == P.epoch;
 }
+// Race stress (the build with ART_RACE_STRESS defined, a test build only):
+// a pseudo-random delay of up to 7 sleeps of 8128 cycles at every point
+// where one workgroup hands data to another or acts on what another handed
+// over, keyed by the call, the group, the chunk and the site, so that the
+// look-back's producers and consumers meet in orders a plain run rarely
+// shows.  Delays only stretch time: every wait stays bounded.
+template <typename Params>
+__device__ __forceinline__ void stress_delay(const Params& P, int gidx, int k, int site) {
+#ifdef ART_RACE_STRESS
+  uint32_t h = (uint32_t)P.epoch * 0x9E3779B1u ^ (uint32_t)gidx * 0x85EBCA77u ^
+               (uint32_t)k * 0xC2B2AE3Du ^ (uint32_t)site * 0x27D4EB2Fu;
+  h ^= h >> 15;
+  h *= 0x2C1B3C6Du;
+  h ^= h >> 12;
+  const uint32_t n = __builtin_amdgcn_readfirstlane((h >> 8) & 7u);
+  for (uint32_t i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(127);
+#else
+  (void)P; (void)gidx; (void)k; (void)site;
+#endif
+}
+
 // The give-up test of one poll of a wait loop (spin counts the polls made).
 template <typename Params>
 __device__ __forceinline__ bool wait_expired(const Params& P, uint32_t spin) {
@@ -660,6 +681,7 @@ __device__ __forceinline__ bool stop_announced_before(const KernelParams& P, int
 // Several chunks of a group may announce; each compare-and-swap that fails
 // saw another announcement land, so the loop ends.  Lane 0 only.
 __device__ void announce_stop(const KernelParams& P, int gidx, int k) {
+  stress_delay(P, gidx, k, 8);
   uint64_t* w = P.stop_word + gidx;
   const uint64_t mine = (P.epoch << kQueueBits) | (uint64_t)k;
   uint64_t cur = ld_relaxed(w);
@@ -747,6 +769,7 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
   // stability state, whose payload replaced the summary in the flag word.
   // Such a state is the fold over every chunk up to it, so the fold restarts
   // from it: the same exact integer result either way.
+  stress_delay(P, gidx, me, 16);
   x = StabState{0, 0, 0, 0};
   if (j >= 0) x = unpack_stab(flag_payload(ld_relaxed(flags + j)));
   for (int i0 = j + 1; i0 < me; i0 += 64) {
@@ -764,6 +787,7 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
 }
 
 __device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, uint32_t state, int lane) {
+  stress_delay(P, gidx, k, 1);
   stores_complete();
   if (lane == 0)
     __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, make_flag(P.epoch, state, 0),
@@ -772,6 +796,7 @@ __device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, 
 // States carried in the flag word itself: one store, no wait.
 __device__ __forceinline__ void publish_word(const KernelParams& P, int gidx, int k, uint32_t state,
                                              uint32_t payload, int lane) {
+  stress_delay(P, gidx, k, 2 + (int)state);
   if (lane == 0)
     __hip_atomic_store(P.flags + (int64_t)gidx * P.max_chunks + k, make_flag(P.epoch, state, payload),
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1010,8 +1035,10 @@ __device__ void resolve_heads(const KernelParams& P, int gidx, int k, const Grou
 
   // entering state per head: the nearest published state, then the
   // summaries after it, folded in order (four chunks' words in flight)
+  stress_delay(P, gidx, k, 11);
   const int j = stab_scan(P, gidx, k, lane);
   if (j == -2) return;
+  stress_delay(P, gidx, k, 12);
   StabState x{0, 0, 0, 0};
   if (mine && j >= 0) {
     const int32_t* w = head_area(P, gidx, j, G) + lane * 8;
@@ -1137,6 +1164,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     j = lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
     if (j == -2) return;
   }
+  stress_delay(P, gidx, k, 9);
   compiler_fence();
   State<G> pre;
   if (j >= 0) {
@@ -1332,6 +1360,7 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
 
   // entering stability state, then this chunk's own
   StabState x;
+  stress_delay(P, gidx, k, 10);
   if (!stab_entering(P, gidx, k, x, lane)) return;
   const bool stopped_before = x.stopped != 0;
   const StabState y = stab_fold(x, sm, t0, P.patience);
@@ -1560,6 +1589,7 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       write_state<G>(blocks + CT * REC + lw * REC, wagg, lane);
     }
     wave_lds_sync();
+    stress_delay(P, gidx, k, 13 + lw);
     if (lane == 0) {
       const int done = __hip_atomic_fetch_add(&s_meta[slot][kMetaDone], 1, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_WORKGROUP);
