@@ -20,7 +20,11 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "art_oracle.c")
-_LIB = os.path.join(_HERE, "libart_oracle.so")
+_DEFAULT_LIB = os.path.join(_HERE, "libart_oracle.so")
+# ART_ORACLE_LIBRARY names another build of the same source (the host-ASan
+# test runs the CPU suite against an AddressSanitizer build)
+_LIB = os.environ.get("ART_ORACLE_LIBRARY") or _DEFAULT_LIB
+ASAN_LIB = os.path.join(_HERE, "libart_oracle_asan.so")
 _lib = None
 
 OK = 0
@@ -47,6 +51,8 @@ class Opts(ctypes.Structure):
 def build(force: bool = True) -> str:
     """Compile the oracle (and the traversal-list oracle, ``oracle.lists``)
     with gcc (-O2, fp-contract off, OpenMP)."""
+    if _LIB != _DEFAULT_LIB:      # another build was named: leave it alone
+        return _LIB
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
@@ -56,6 +62,17 @@ def build(force: bool = True) -> str:
     from . import lists
     lists.build(force=force)
     return _LIB
+
+
+def build_asan() -> tuple:
+    """AddressSanitizer builds of the oracle and the list oracle (gcc; the
+    process that loads them preloads gcc's libasan)."""
+    from . import lists
+    flags = ["gcc", "-O1", "-g", "-std=c11", "-fPIC", "-shared", "-fno-omit-frame-pointer",
+             "-fsanitize=address", "-ffp-contract=off", "-Wall"]
+    subprocess.check_call([*flags, "-fopenmp", "-o", ASAN_LIB, _SRC, "-lm"])
+    subprocess.check_call([*flags, "-o", lists.ASAN_LIB, lists._SRC, "-lm"])
+    return ASAN_LIB, lists.ASAN_LIB
 
 
 def load_library(path: str):

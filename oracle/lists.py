@@ -16,7 +16,9 @@ from . import _bits, _i32, _ptr
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "art_list_oracle.c")
-_LIB = os.path.join(_HERE, "libart_list_oracle.so")
+_DEFAULT_LIB = os.path.join(_HERE, "libart_list_oracle.so")
+_LIB = os.environ.get("ART_LIST_ORACLE_LIBRARY") or _DEFAULT_LIB
+ASAN_LIB = os.path.join(_HERE, "libart_list_oracle_asan.so")
 _lib = None
 
 IMPORTANCE, STREAMING = 0, 1
@@ -36,6 +38,8 @@ class ListOpts(ctypes.Structure):
 
 
 def build(force: bool = True) -> str:
+    if _LIB != _DEFAULT_LIB:      # another build was named: leave it alone
+        return _LIB
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",

@@ -5,7 +5,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libart.so")
+# ART_LIBRARY names another build of the same sources (the host-ASan test
+# runs the CPU suite against the AddressSanitizer build); default in-tree
+LIB_PATH = os.environ.get("ART_LIBRARY") or os.path.join(HERE, "libart.so")
 
 OK = 0
 ERR_INVALID_ARG = 1
