@@ -83,3 +83,26 @@ def test_delayed_handovers_keep_the_sequential_result(stress_lib, case):
             rep = compare_per_head(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2], host=host,
                                    name="race_stress_per_head")
             assert rep.ok(), f"per head, thr {thr}: {rep}"
+
+
+def test_the_stress_build_delays(stress_lib):
+    """The delays are really there: the same one-block-chunk call takes
+    clearly longer through the stress build than through the library."""
+    import time
+    wl = _to_dev(small_workload(95, batch=2, kv_heads=2, group=4, seq_len=(9000, 6000), needles=4))
+    ws = api.new_workspace(64 << 20, DEV)
+
+    def timed():
+        ts = []
+        for _ in range(5):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            api.decode_workload(wl, tau=0.0, phi=1e-4, patience=5, chunk_blocks=1, workspace=ws)
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        return sorted(ts)[2]
+    plain = timed()
+    with _lib.using(stress_lib):
+        stressed = timed()
+    _say(f"  one call: library {plain * 1e6:.0f} us, stress build {stressed * 1e6:.0f} us")
+    assert stressed > 2 * plain
