@@ -36,6 +36,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, published
 HEADLINE = "qwen3_32b_ragged"
+# windows of the bounded-speculation runs reported for the other workloads
+BOUNDED_WINDOWS = (2, 4, 8)
 # the ragged batch's thresholds: the middle of the swept set (tau = phi)
 HEADLINE_THRESHOLDS = {"qwen3_32b_ragged": (1e-3, 1e-3)}
 
@@ -46,15 +48,26 @@ HEADLINE_THRESHOLDS = {"qwen3_32b_ragged": (1e-3, 1e-3)}
 # SHA-256; after any change to those sources the figure is reported as null
 # until it is counted again.
 COUNTED_TRAFFIC = {
-    "sources_sha256": "66a0abb1b1426461e830bd40be927657a410f307925adc755b27bd932dcfb32e",
-    "bytes": {("qwen3_32b_ragged", 1e-3, 1e-3, "on"): 5713209112,
-              ("qwen3_32b_ragged", 0.0, 1e-3, "off"): 5723955352,
-              ("llama3_8b_32k", 1e-3, 1e-4, "on"): 535206800,
-              ("llama3_8b_32k", 0.0, 1e-4, "off"): 1120636696,
-              ("sparse25_128k", 1e-3, 1e-4, "on"): 261530072,
-              ("sparse25_128k", 0.0, 1e-4, "off"): 561813320,
-              ("long_512k", 1e-3, 1e-4, "on"): 637601328,
-              ("long_512k", 0.0, 1e-4, "off"): 2191666272},
+    "sources_sha256": "9f022b246c286b231e4c7745cee7063daebf8a5f43e6a97b8b73bf1d968ed2ff",
+    "bytes": {('qwen3_32b_ragged', 0.001, 0.001, 'on'): 5706164768,
+              ('qwen3_32b_ragged', 0.0, 0.001, 'off'): 5718489848,
+              ('llama3_8b_32k', 0.001, 0.0001, 'on'): 536734160,
+              ('llama3_8b_32k', 0.0, 0.0001, 'off'): 1120267976,
+              ('sparse25_128k', 0.001, 0.0001, 'on'): 255790648,
+              ('sparse25_128k', 0.0, 0.0001, 'off'): 561815960,
+              ('long_512k', 0.001, 0.0001, 'on'): 640954856,
+              ('long_512k', 0.0, 0.0001, 'off'): 2191738384,
+              ('tiny_4k', 0.001, 0.0001, 'on'): 5430944,
+              ('tiny_4k', 0.0, 0.0001, 'off'): 5385744,
+              ('llama3_8b_32k', 0.001, 0.0001, 'on_ahead2'): 304161416,
+              ('llama3_8b_32k', 0.001, 0.0001, 'on_ahead4'): 340129088,
+              ('llama3_8b_32k', 0.001, 0.0001, 'on_ahead8'): 412773488,
+              ('sparse25_128k', 0.001, 0.0001, 'on_ahead2'): 37507712,
+              ('sparse25_128k', 0.001, 0.0001, 'on_ahead4'): 57143120,
+              ('sparse25_128k', 0.001, 0.0001, 'on_ahead8'): 94963904,
+              ('long_512k', 0.001, 0.0001, 'on_ahead2'): 192792960,
+              ('long_512k', 0.001, 0.0001, 'on_ahead4'): 198902304,
+              ('long_512k', 0.001, 0.0001, 'on_ahead8'): 217208592},
 }
 TRAFFIC_SOURCES = ("art_kernels.hip", "art_api.cpp", "art_internal.h")
 
@@ -98,6 +111,8 @@ def parse():
     ap.add_argument("--phi", type=float, default=None)
     ap.add_argument("--patience", type=int, default=None)
     ap.add_argument("--chunk-blocks", type=int, default=0)
+    ap.add_argument("--max-ahead", type=int, default=0,
+                    help="bound the chunks read ahead of the last tested one (0 = unbounded)")
     ap.add_argument("--no-detector", action="store_true",
                     help="the headline mode without the stability test (full attention)")
     ap.add_argument("--list-producer", action="store_true",
@@ -125,7 +140,7 @@ class Runner:
     can check afterwards that every call stopped every group alike."""
 
     def __init__(self, wl, copies, tau, phi, patience, chunk_blocks, no_detector=False,
-                 n_stop_bufs=1):
+                 n_stop_bufs=1, max_ahead=0):
         import torch
         from paper_2606_00024_amd import _lib, api
         self._lib = _lib
@@ -136,7 +151,8 @@ class Runner:
                                     block_size=s.block_size, block_list=wl.block_list)
         self.opts = api.make_opts(softmax_scale=s.softmax_scale, tau=tau, phi=phi,
                                   patience=patience, dense_order=s.dense_order,
-                                  chunk_blocks=chunk_blocks, no_detector=no_detector)
+                                  chunk_blocks=chunk_blocks, no_detector=no_detector,
+                                  max_ahead_chunks=max_ahead)
         dev = wl.q.device
         B, Hq, D = wl.q.shape
         self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
@@ -240,12 +256,14 @@ def time_steps(runner, steps, warmup):
 
 
 def measure(wl, tau, phi, pat, steps, warmup, copies, chunk_blocks=0, no_detector=False,
-            keep_out=False):
+            keep_out=False, max_ahead=0):
     """One mode of one workload: kernel time, rates, skipped share."""
     import torch
-    run = Runner(wl, copies, tau, phi, pat, chunk_blocks, no_detector, n_stop_bufs=steps)
+    run = Runner(wl, copies, tau, phi, pat, chunk_blocks, no_detector, n_stop_bufs=steps,
+                 max_ahead=max_ahead)
     print(f"[bench] {wl.spec.name}: tau={tau} phi={phi} p={pat} steps={steps}"
-          f"{' no_detector' if no_detector else ''}", file=sys.stderr, flush=True)
+          f"{' no_detector' if no_detector else ''}"
+          f"{f' max_ahead={max_ahead}' if max_ahead else ''}", file=sys.stderr, flush=True)
     wall, kern_ms, spread = time_steps(run, steps, warmup)
     alg, read_tokens, blocks = algorithmic_bytes(wl, run.stop)
     total_blocks = sum(map(sum, wl.traversal_lengths()))
@@ -494,10 +512,11 @@ def main():
     ceiling = None if (args.no_extra or args.only_headline) else read_ceiling()
 
     on, out_on = measure(wl, tau, phi, pat, args.steps, args.warmup, copies, args.chunk_blocks,
-                         args.no_detector, keep_out=True)
+                         args.no_detector, keep_out=True, max_ahead=args.max_ahead)
     if args.only_headline:
         print(json.dumps({"workload": spec.name, "tau": tau, "phi": phi, "patience": pat,
-                          "no_detector": args.no_detector, **on}), flush=True)
+                          "no_detector": args.no_detector, "max_ahead": args.max_ahead, **on}),
+              flush=True)
         return
     off = None
     out_full = None
@@ -505,7 +524,7 @@ def main():
         off, out_full = measure(wl, 0.0, phi, pat, max(10, args.steps // 2),
                                 max(5, args.warmup // 2), copies, args.chunk_blocks, keep_out=True)
     defaults = (tau, phi, pat) == thresholds(spec) and args.chunk_blocks == 0 \
-        and not args.no_detector
+        and not args.no_detector and args.max_ahead == 0
 
     def roofline(r, key):
         ach = r["hbm_gbps_on_bytes_read"]
@@ -567,6 +586,14 @@ def main():
                 entry[mode]["traffic"] = counted_traffic(key)
                 if ceiling is not None:
                     entry[mode]["frac_of_measured_read"] = r["hbm_gbps_on_bytes_read"] / ceiling["gbps"]
+            # bounded speculation (max_ahead_chunks), termination on: the
+            # same results, fewer reads past the stops, possibly idle workgroups
+            entry["on_max_ahead"] = {}
+            for wnd in BOUNDED_WINDOWS:
+                r_b, _ = measure(owl, ot, of, op, 40, 10, oc, max_ahead=wnd)
+                entry["on_max_ahead"][str(wnd)] = {
+                    "kernel_ms": r_b["kernel_ms"], "skipped_pct": r_b["skipped_pct"],
+                    "traffic": counted_traffic((name, ot, of, f"on_ahead{wnd}"))}
             others[name] = entry
             del owl
             torch.cuda.empty_cache()

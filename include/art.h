@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define ART_ABI_VERSION 7
+#define ART_ABI_VERSION 8
 
 typedef enum {
     ART_OK = 0,
@@ -146,6 +146,15 @@ typedef struct {
                                       stops).  A group reads blocks until its last head
                                       has stopped.  Needs a larger workspace
                                       (art_decode_workspace_bytes) */
+    int32_t max_ahead_chunks;      /* 0 = unbounded; n > 0 bounds the reads past a stop:
+                                      chunk k of a traversal is not loaded before chunk
+                                      k - n of it has been through the stability test
+                                      (or a stop before chunk k is known), so at most n
+                                      chunks are read past the one that decides the stop.
+                                      It changes which blocks are read, never the
+                                      results (the outputs are bit for bit those of the
+                                      unbounded call); it can idle workgroups, so the
+                                      launch may take longer */
 } art_decode_opts;
 
 /* Version of this ABI (ART_ABI_VERSION). */

@@ -45,7 +45,7 @@ class DecodeShape(ctypes.Structure):
 
 
 # ART_ABI_VERSION of include/art.h that these structure layouts follow
-ABI_VERSION = 7
+ABI_VERSION = 8
 
 
 class DecodeOpts(ctypes.Structure):
@@ -54,7 +54,8 @@ class DecodeOpts(ctypes.Structure):
                 ("dense_order", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
                 ("chunk_blocks", ctypes.c_int32), ("probe_stride", ctypes.c_int32),
                 ("scale_of_accumulator", ctypes.c_int32), ("no_detector", ctypes.c_int32),
-                ("max_wait_polls", ctypes.c_int32), ("per_head_stop", ctypes.c_int32)]
+                ("max_wait_polls", ctypes.c_int32), ("per_head_stop", ctypes.c_int32),
+                ("max_ahead_chunks", ctypes.c_int32)]
 
 
 class ListOpts(ctypes.Structure):

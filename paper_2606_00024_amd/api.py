@@ -54,7 +54,7 @@ def make_opts(*, softmax_scale: float, tau: float, phi: float, patience: int,
               dense_order: int = 0, out_dtype=torch.float32, chunk_blocks: int = 0,
               probe_stride: int = 1, scale_of_accumulator: bool = False,
               no_detector: bool = False, max_wait_polls: int = 0,
-              per_head_stop: bool = False) -> DecodeOpts:
+              per_head_stop: bool = False, max_ahead_chunks: int = 0) -> DecodeOpts:
     od = _lib.OUT_BF16 if out_dtype == torch.bfloat16 else _lib.OUT_F32
     if out_dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_dtype must be float32 or bfloat16")
@@ -64,7 +64,8 @@ def make_opts(*, softmax_scale: float, tau: float, phi: float, patience: int,
                       scale_of_accumulator=1 if scale_of_accumulator else 0,
                       no_detector=1 if no_detector else 0,
                       max_wait_polls=int(max_wait_polls),
-                      per_head_stop=1 if per_head_stop else 0)
+                      per_head_stop=1 if per_head_stop else 0,
+                      max_ahead_chunks=int(max_ahead_chunks))
 
 
 def workspace_bytes(shape: DecodeShape, opts: DecodeOpts) -> int:
@@ -100,6 +101,7 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                      chunk_blocks: int = 0, probe_stride: int = 1,
                      scale_of_accumulator: bool = False, no_detector: bool = False,
                      max_wait_polls: int = 0, per_head_stop: bool = False,
+                     max_ahead_chunks: int = 0,
                      workspace: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      stop_block: Optional[torch.Tensor] = None):
@@ -117,7 +119,9 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     reports ART_ERR_DEVICE_TIMEOUT through ``workspace_status``).
     ``per_head_stop`` gives every query head its own patience counter and stop
     (out and lse at the head's own stop; stop_block is then [B][Hq], each
-    head's stop).
+    head's stop).  ``max_ahead_chunks`` n > 0 bounds the reads past a stop:
+    a chunk of a traversal is loaded only once the chunk n before it has been
+    through the stability test (the results are the same bits).
     """
     _require_cuda(q, "q", torch.bfloat16)
     _require_cuda(k_cache, "k_cache", torch.bfloat16)
@@ -143,7 +147,7 @@ def decode_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                      dense_order=dense_order, out_dtype=out_dtype, chunk_blocks=chunk_blocks,
                      probe_stride=probe_stride, scale_of_accumulator=scale_of_accumulator,
                      no_detector=no_detector, max_wait_polls=max_wait_polls,
-                     per_head_stop=per_head_stop)
+                     per_head_stop=per_head_stop, max_ahead_chunks=max_ahead_chunks)
     dev = q.device
     if out is None:
         out = torch.empty((B, Hq, D), dtype=out_dtype, device=dev)

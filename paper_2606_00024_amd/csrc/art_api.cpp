@@ -75,7 +75,7 @@ art_status check_shape(const art_decode_shape* s, const art_decode_opts* o) {
         (o->probe_stride > 1 && s->head_dim % o->probe_stride != 0) ||
         (o->scale_of_accumulator != 0 && o->scale_of_accumulator != 1) ||
         (o->no_detector != 0 && o->no_detector != 1) || o->max_wait_polls < 0 ||
-        (o->per_head_stop != 0 && o->per_head_stop != 1))
+        (o->per_head_stop != 0 && o->per_head_stop != 1) || o->max_ahead_chunks < 0)
         return ART_ERR_INVALID_ARG;
     const int g = s->num_q_heads / s->num_kv_heads;
     if (s->head_dim != art::kHeadDim) return ART_ERR_UNSUPPORTED;
@@ -280,6 +280,7 @@ art_status enqueue_decode(const Plan& plan, const art_decode_shape* shape,
     k.head_area = reinterpret_cast<int32_t*>(ws + plan.ws.head_off);
     k.epoch = next_epoch();
     k.spin_limit = opts->max_wait_polls > 0 ? (uint32_t)opts->max_wait_polls : kSpinLimit;
+    k.max_ahead = opts->max_ahead_chunks;
     if (k.epoch >= (uint64_t(1) << 40)) return ART_ERR_UNSUPPORTED;
     return art::launch_decode(plan, k, stream) == (int)hipSuccess ? ART_OK : ART_ERR_HIP;
 }

@@ -103,6 +103,7 @@ struct KernelParams {
     int32_t* head_area;      // per-head mode: [groups][max_chunks][g][8] int32
     uint64_t epoch;          // unique per call; tags every flag it writes
     uint32_t spin_limit;     // polls before a wait gives up
+    int32_t max_ahead;       // 0, or chunks a load may run ahead of the last tested chunk
 };
 
 // Launchers (art_kernels.hip).  Return a hipError_t.

@@ -1537,6 +1537,23 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
       // tiles are fetched together once per chunk: lane 4m + n covers
       // 16-token group n of the wave's m-th tile (at most 16 tiles per wave).
       const int n_my = lw < nb ? (nb - lw + kLoaders - 1) / kLoaders * tpb : 0;
+      // Bounded speculation: chunk k waits until chunk k - max_ahead of the
+      // group has been through the stability test (its summary, or its
+      // inclusive state without the test), unless a stop before chunk k is
+      // announced meanwhile.  The waited-on chunk was claimed earlier, so
+      // it makes progress without this one.
+      if (P.max_ahead > 0 && k >= P.max_ahead) {
+        const uint64_t* fw = P.flags + (int64_t)gidx * P.max_chunks + (k - P.max_ahead);
+        const uint32_t need = P.no_detector ? kInclusive : kStabSummary;
+        for (uint32_t spin = 0;; ++spin) {
+          if (flag_state(ld_relaxed(fw), P.epoch) >= need) break;
+          if (stop_announced_before(P, gidx, k) || wait_expired(P, spin)) {
+            aborted = true;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+      }
       // the stop word travels with the page reads: a chunk that lies after
       // an announced stop is given up before any tile is loaded
       const uint64_t sw0 = ld_relaxed(P.stop_word + gidx);

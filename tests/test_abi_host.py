@@ -94,7 +94,7 @@ def test_shape_errors(lib, kw, status):
     dict(softmax_scale=float("inf")), dict(probe_stride=-1), dict(probe_stride=3),
     dict(probe_stride=6), dict(probe_stride=256), dict(scale_of_accumulator=2),
     dict(no_detector=-1), dict(no_detector=2), dict(max_wait_polls=-1),
-    dict(per_head_stop=2), dict(per_head_stop=-1),
+    dict(per_head_stop=2), dict(per_head_stop=-1), dict(max_ahead_chunks=-1),
 ])
 def test_option_errors(lib, kw):
     n, st = _ws(_shape(), _opts(**kw))

@@ -99,3 +99,13 @@ def test_more_than_one_gpu_is_refused_before_any_gpu_work():
     assert r.returncode == 2
     assert "one GPU only" in r.stderr
     assert r.stdout == ""
+
+
+def test_counted_traffic_is_current():
+    """The committed counts were taken on the sources as they stand: a kernel
+    or host change must come with a recount (else bench reports null)."""
+    assert bench.COUNTED_TRAFFIC["sources_sha256"] == bench.sources_digest()
+    for w in ("qwen3_32b_ragged", "llama3_8b_32k", "sparse25_128k", "long_512k"):
+        tau, phi, _ = bench.thresholds(W.WORKLOADS[w])
+        assert bench.counted_traffic((w, tau, phi, "on")) is not None
+        assert bench.counted_traffic((w, 0.0, phi, "off")) is not None
