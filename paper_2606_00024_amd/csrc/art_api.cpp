@@ -107,10 +107,15 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
 
     // LDS of a workgroup: two or three chunk buffers of C*tpb tile records
     // plus three per-loader partial aggregates each (when they fit), and
-    // three V staging buffers (32 rows of 288 bytes).  Kept within 78 KiB,
-    // so that two workgroups share a CU's 160 KiB.
+    // three V staging buffers: half tiles (32 rows of 288 bytes) for groups
+    // of up to 4 heads, quarter tiles (4 KiB) for 8 or more.  A record of 8
+    // or more heads holds 4 KiB of outputs, so when every block is one tile
+    // the loaders stage V in the record the tile is about to write, and the
+    // staging buffers go.
+    // Kept within 78 KiB, so that two workgroups share a CU's 160 KiB.
     const size_t rec_bytes = (size_t)(g * art::kHeadDim + 2 * g) * 4;
-    const size_t pbuf_bytes = (size_t)3 * 32 * 288 + 16;
+    const bool v_in_record = g >= 8 && tpb == 1;
+    const size_t pbuf_bytes = v_in_record ? 0 : (g >= 8 ? (size_t)3 * 4096 : (size_t)3 * 32 * 288) + 16;
     const size_t lds_cap = 78 * 1024;
     auto lds_for = [&](int blocks, int partials, int slots = 2) {
         return slots * (size_t)(blocks + partials) * rec_bytes + pbuf_bytes;
@@ -168,6 +173,7 @@ art_status make_plan(const art_decode_shape* s, const art_decode_opts* o, Plan* 
     p->t_cap = (int32_t)t_cap;
     p->record_floats = (g * art::kHeadDim + 2 * g + 63) / 64 * 64;
     p->loader_partials = partials;
+    p->v_in_record = v_in_record ? 1 : 0;
     // (a third buffer was measured: it lets loaders run further past a
     // stop and gains nothing elsewhere)
     p->slots = 2;
@@ -261,6 +267,7 @@ art_status enqueue_decode(const Plan& plan, const art_decode_shape* shape,
     k.record_floats = plan.record_floats;
     k.chunk_recs_lds = plan.chunk_blocks;
     k.loader_partials = plan.loader_partials;
+    k.v_in_record = plan.v_in_record;
     k.q = static_cast<const uint16_t*>(q);
     k.k = static_cast<const uint16_t*>(k_cache);
     k.v = static_cast<const uint16_t*>(v_cache);

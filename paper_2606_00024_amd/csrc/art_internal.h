@@ -57,6 +57,7 @@ struct Plan {
     int32_t t_cap;           // traversal length bound per group
     int32_t record_floats;   // floats per aggregate / inclusive record
     int32_t loader_partials; // see KernelParams
+    int32_t v_in_record;     // see KernelParams
     int32_t slots;           // chunk buffers in LDS (2 or 3)
     size_t lds_bytes;        // dynamic LDS per workgroup
     WorkspaceLayout ws;
@@ -83,6 +84,7 @@ struct KernelParams {
     int32_t chunk_recs_lds;  // block records per LDS chunk buffer
     int32_t loader_partials; // per-loader partial aggregates kept in LDS (3 or 0)
     int32_t n_slots;         // chunk buffers in LDS (2 or 3)
+    int32_t v_in_record;     // 1: V is staged in the LDS record being written (no staging buffers)
     // data
     const uint16_t* q;
     const uint16_t* k;

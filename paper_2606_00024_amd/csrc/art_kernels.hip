@@ -403,16 +403,28 @@ __device__ __forceinline__ int clamp_page(const KernelParams& P, int b, int tok)
 //     each lane ends up holding the probabilities of one head for exactly
 //     the eight tokens that the P.V A-operand needs from it;
 //   - P.V with P as A (heads x 32 tokens) and V as B (32 tokens x 16 dims).
-//     V reaches the B layout (eight tokens of one dim per lane) through LDS:
-//     each half tile is written row-major and read back with
-//     ds_read_b64_tr_b16.  P is split into three bf16 parts (hi + mid + lo
-//     carries 24 significant bits), so P.V keeps fp32 precision.
+//     V reaches the B layout (eight tokens of one dim per lane) through LDS,
+//     written row-major and read back with ds_read_b64_tr_b16: for groups
+//     of up to 4 heads, half tiles through the loader's own staging buffer;
+//     for 8 or more, quarter tiles (16 tokens, 4 KiB), through the output
+//     part of the very record the tile is about to write when every block
+//     is one tile (nothing reads it before the record is written, and the
+//     LDS so saved holds longer chunks), else through a 4 KiB staging
+//     buffer.  P is split into three bf16 parts (hi +
+//     mid + lo carries 24 significant bits), so P.V keeps fp32 precision.
 // The record written to LDS holds the normalised block output
 // sum_j p_hj v_j / l_h [G][128], m_h [G] (base 2) and l_h [G].  pg[n] is the
 // (uniform) physical page of 16-token group n.
 typedef short v4i16 __attribute__((ext_vector_type(4)));
-constexpr int kVPitch = 144;                  // u16 per row of the V staging buffer (288 B)
+constexpr int kVPitch = 144;                  // u16 per row of a staging buffer (288 B)
 constexpr int kVBufU16 = 32 * kVPitch;        // one half tile: 32 rows
+constexpr int kVRow = 128;                    // u16 per row of a quarter-tile stage (256 B)
+// Quarter-tile stage: row r's 16-byte piece j sits at piece j ^ 2(r & 3),
+// so that the four rows one transposing read touches fall on distinct banks
+// (a half-tile buffer pads its rows to 288 bytes for the same end).
+__device__ __forceinline__ int vstage_off(int row, int piece) {
+  return row * kVRow + ((piece ^ (2 * (row & 3))) << 3);
+}
 
 // The first tile of a block writes the block record; each later tile of
 // the block (accumulate) is folded into it: both parts rescaled to the
@@ -536,50 +548,82 @@ __device__ void compute_tile(const KernelParams& P, int kvh, int L, int tok0, co
   // P.V over the two halves of the tile.  B for K-step c and dims
   // 16d .. 16d+15: lane (lo, g) needs V[token of element e][16d + lo]; in
   // each 16-lane group, source lane 4k + q of a transposing read points at
-  // row 4g + k (then 16 + 4g + k), columns 16d + 4q .. +3.  The row pitch of
-  // 288 bytes puts the 16 lanes of a group on 32 distinct banks.
+  // row 4g + k of a 16-row quarter (then of the next one), columns
+  // 16d + 4q .. +3.
   f32x4 acc[8];
 #pragma unroll
   for (int d = 0; d < 8; ++d) acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int rk = lo >> 2, cq = lo & 3;
+  if constexpr (G >= 8) {
+    // a quarter at a time, the first quarter's B parts (elements 0..3) kept
+    // in registers until the second's are read
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < 2; ++c) {
+      v4i16 r0[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<u32x4*>(vbuf + (4 * i + g) * kVPitch + 8 * lo) = vr[8 * c + i];
-    wave_lds_sync();
+      for (int qh = 0; qh < 2; ++qh) {
 #pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      const v4i16 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) v4i16*)(vbuf + (4 * g + rk) * kVPitch + 16 * d + 4 * cq));
-      const v4i16 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) v4i16*)(vbuf + (16 + 4 * g + rk) * kVPitch + 16 * d + 4 * cq));
-      const bf16x8 b = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
+        for (int i = 0; i < 4; ++i)
+          *reinterpret_cast<u32x4*>(vbuf + vstage_off(4 * i + g, lo)) = vr[8 * c + 4 * qh + i];
+        wave_lds_sync();
 #pragma unroll
-      for (int j = 0; j < 3; ++j) acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[c][j], b, acc[d], 0, 0, 0);
+        for (int d = 0; d < 8; ++d) {
+          const v4i16 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4i16*)(vbuf + vstage_off(4 * g + rk, 2 * d + (cq >> 1)) +
+                                                         4 * (cq & 1)));
+          if (qh == 0) {
+            r0[d] = r;
+          } else {
+            const bf16x8 b = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0[d], r, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+            for (int j = 0; j < 3; ++j) acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[c][j], b, acc[d], 0, 0, 0);
+          }
+        }
+        wave_lds_sync();  // the reads of this quarter complete before the next one is written
+      }
     }
-    wave_lds_sync();  // the reads of this half complete before the next half is written
+  } else {
+    // a whole half at a time; the row pitch of 288 bytes puts the 16 lanes
+    // of a group on 32 distinct banks
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        *reinterpret_cast<u32x4*>(vbuf + (4 * i + g) * kVPitch + 8 * lo) = vr[8 * c + i];
+      wave_lds_sync();
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        const v4i16 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16*)(vbuf + (4 * g + rk) * kVPitch + 16 * d + 4 * cq));
+        const v4i16 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16*)(vbuf + (16 + 4 * g + rk) * kVPitch + 16 * d + 4 * cq));
+        const bf16x8 b = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int j = 0; j < 3; ++j) acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[c][j], b, acc[d], 0, 0, 0);
+      }
+      wave_lds_sync();  // the reads of this half complete before the next half is written
+    }
   }
-  // acc[d][r]: head 4g + r, dim 16d + lo.  Row 0 of the lanes (g = 0) holds
-  // (m, l) of head lo; it leaves the factors that normalise (or fold) the
-  // tile's sums in the staging buffer, which the P.V loop no longer reads.
-  float* scale = reinterpret_cast<float*>(vbuf);
+  // acc[d][r]: head 4g + r, dim 16d + lo.  A block's first tile divides
+  // its sums by the mass l_h written to the record above; a later tile's
+  // fold factors come from row 0 of the lanes (g = 0, head lo) through the
+  // staging buffer, which the P.V loop no longer reads (a record never
+  // stages its own later tiles: records stage only blocks of one tile).
   if (!accumulate) {
-    if (g == 0 && lo < G) scale[lo] = ls > 0.f ? fast_rcp(ls) : 0.f;
-    wave_lds_sync();
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int h = 4 * g + r;
       if (h < G) {
-        const float inv = scale[h];
+        const float l = rec[G * kD + G + h];
+        const float inv = l > 0.f ? fast_rcp(l) : 0.f;
 #pragma unroll
         for (int d = 0; d < 8; ++d) rec[h * kD + 16 * d + lo] = __fmul_rn(acc[d][r], inv);
       }
     }
-    wave_lds_sync();  // the factors are read before the buffer is reused
     return;
   }
   // fold into the block record: o = (o_rec L_rec so + sum_tile sn) / L_new
+  float* scale = reinterpret_cast<float*>(vbuf);
   if (g == 0 && lo < G) {
     const float mo = rec[G * kD + lo], lo_sum = rec[G * kD + G + lo];
     const float mn = fmaxf(mo, mx);
@@ -1440,7 +1484,9 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
 
   // ---------------- loaders ----------------
   const int lw = wave - 1;
-  uint16_t* vbuf = vbuf_all + lw * kVBufU16;
+  // (a loader's own staging buffer: a half tile, or a quarter tile for 8 or
+  // more heads; unused when V is staged in the records)
+  uint16_t* vbuf = vbuf_all + lw * (G >= 8 ? 16 * kVRow : kVBufU16);
   // leader: the queue it claims from (its own first, then the others in
   // turn once its own is used up) and the queues found used up
   int qx = blockIdx.x % kQueues;
@@ -1585,7 +1631,9 @@ __global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams
         const int tok0 = __builtin_amdgcn_readlane(my_tok0, 4 * m);
         const int pg[4] = {__builtin_amdgcn_readlane(my_page, 4 * m), __builtin_amdgcn_readlane(my_page, 4 * m + 1),
                            __builtin_amdgcn_readlane(my_page, 4 * m + 2), __builtin_amdgcn_readlane(my_page, 4 * m + 3)};
-        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa, vbuf, blocks + i * REC, j > 0);
+        compute_tile<G>(P, gi.kvh, gi.L, tok0, pg, qa,
+                        P.v_in_record ? reinterpret_cast<uint16_t*>(blocks + i * REC) : vbuf,
+                        blocks + i * REC, j > 0);
         if (stop_word_before(sw, P.epoch, k)) {
           aborted = true;
           break;

@@ -72,6 +72,8 @@ SMALL = [
     (7, 3, 1, 4, (1, 65, 640), 64, 16, 0, False),
     (8, 1, 4, 4, 5000, 256, 256, 0, False),
     (9, 2, 2, 4, (3000, 777), 128, 16, 0, True),
+    (10, 2, 2, 8, (1500, 3100), 128, 64, 0, False),
+    (11, 1, 2, 16, 2600, 256, 128, 1, True),
 ]
 
 
