@@ -85,6 +85,7 @@ struct KernelParams {
     int32_t loader_partials; // per-loader partial aggregates kept in LDS (3 or 0)
     int32_t n_slots;         // chunk buffers in LDS (2 or 3)
     int32_t v_in_record;     // 1: V is staged in the LDS record being written (no staging buffers)
+    int32_t look_first;      // 1: a chunk looks back once before publishing its aggregate (set at launch)
     // data
     const uint16_t* q;
     const uint16_t* k;

@@ -765,6 +765,24 @@ __device__ int lookback_scan(const KernelParams& P, int gidx, int me, uint32_t n
   return -1;
 }
 
+// One pass of lookback_scan with no wait: the index found, -1 for an empty
+// prefix, or -3 when a chunk in the way has not published yet.
+__device__ int lookback_once(const KernelParams& P, int gidx, int me, uint32_t need_lo,
+                             uint32_t need_hi, int lane) {
+  const uint64_t* flags = P.flags + (int64_t)gidx * P.max_chunks;
+  for (int hi = me - 1; hi >= 0; hi -= 64) {
+    const int idx = hi - lane;
+    const uint32_t st = idx >= 0 ? flag_state(ld_relaxed(flags + idx), P.epoch) : 0u;
+    const uint64_t have_hi = __ballot(idx >= 0 && st >= need_hi);
+    const uint64_t have_lo = __ballot(idx < 0 || st >= need_lo);
+    const int first = have_hi ? __ffsll((unsigned long long)have_hi) - 1 : 64;
+    const uint64_t need = first >= 64 ? ~0ull : ((1ull << first) - 1ull);
+    if ((have_lo & need) != need) return -3;
+    if (first < 64) return hi - first;
+  }
+  return -1;
+}
+
 // States whose data sits in the workspace records: the flag goes out once
 // the record stores have completed.
 // Stability state on entering chunk `me` of group gidx: the nearest chunk j
@@ -1203,9 +1221,25 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
   } else if (flag_state(prev_flag, P.epoch) >= kInclusive) {
     j = k - 1;
   } else {
-    publish_state<G>(rs, rec_agg, agg, lane);
-    publish(P, gidx, k, kAggregate, lane);
-    j = lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
+    // With few chunks of a group in flight (look_first), one pass over the
+    // flags often finds the prefix complete, and the aggregate record, one
+    // of the two written per chunk, is not needed by anyone; with many, the
+    // later chunks need it at once to fold past this one.
+    // (compiled for 8 or more heads only: the launches that pass the gate
+    // are those of many groups of 8, and the extra code alone measurably
+    // slowed the instances for smaller groups)
+    if (G >= 8 && P.look_first) {
+      j = lookback_once(P, gidx, k, kAggregate, kInclusive, lane);
+      if (j == -3) {
+        publish_state<G>(rs, rec_agg, agg, lane);
+        publish(P, gidx, k, kAggregate, lane);
+        j = lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
+      }
+    } else {
+      publish_state<G>(rs, rec_agg, agg, lane);
+      publish(P, gidx, k, kAggregate, lane);
+      j = lookback_scan(P, gidx, k, kAggregate, kInclusive, lane);
+    }
     if (j == -2) return;
   }
   stress_delay(P, gidx, k, 9);
@@ -1684,9 +1718,17 @@ int launch_g(const Plan& plan, const KernelParams& params, hipStream_t stream) {
   // nothing but reads past their stops.
   const int64_t per_groups = max((int64_t)cus, (int64_t)32 * plan.n_groups);
   const int64_t grid = min(work, min((int64_t)cus * per_cu, per_groups));
+  // Chunks of one group in flight at once: about the launch's chunk buffers
+  // over the groups.  Up to 8 (many groups), a chunk of a group of 8 or
+  // more heads looks back before it publishes its aggregate (measured: -2 %
+  // on 256 groups of g = 8, +5 to +13 % with 32 or more buffers per group).
+  // A function of the shape and the device only; the results are the same
+  // bits either way.
+  KernelParams p = params;
+  p.look_first = grid * plan.slots <= (int64_t)8 * plan.n_groups ? 1 : 0;
   auto kernel = art_decode_kernel<G, PH>;
   hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kThreads),
-                     plan.lds_bytes, stream, params);
+                     plan.lds_bytes, stream, p);
   return (int)hipGetLastError();
 }
 

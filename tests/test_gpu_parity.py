@@ -74,6 +74,9 @@ SMALL = [
     (9, 2, 2, 4, (3000, 777), 128, 16, 0, True),
     (10, 2, 2, 8, (1500, 3100), 128, 64, 0, False),
     (11, 1, 2, 16, 2600, 256, 128, 1, True),
+    # 128 groups of a few chunks: few chunks of a group in flight, so a chunk
+    # looks back once before it publishes its aggregate
+    (12, 32, 4, 4, 1500, 64, 64, 0, False),
 ]
 
 

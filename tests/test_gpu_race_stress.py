@@ -85,6 +85,25 @@ def test_delayed_handovers_keep_the_sequential_result(stress_lib, case):
             assert rep.ok(), f"per head, thr {thr}: {rep}"
 
 
+def test_look_first_under_delays(stress_lib):
+    """128 groups of a few chunks each: the launch holds few chunks of a
+    group at once, and a chunk then looks back once before it publishes its
+    aggregate.  Delayed hand-overs must not change the result."""
+    wl = _to_dev(small_workload(96, batch=32, kv_heads=4, group=4, seq_len=1500, needles=2))
+    host = host_copy(wl)
+    ws = api.new_workspace(64 << 20, DEV)
+    with _lib.using(stress_lib):
+        for thr in THRESHOLDS:
+            for chunk in (0, 1):
+                _say(f"  stress call s96 thr={thr} chunk={chunk}")
+                gpu = api.decode_workload(wl, tau=thr[0], phi=thr[1], patience=thr[2],
+                                          chunk_blocks=chunk, workspace=ws)
+                assert api.workspace_status(ws) == _lib.OK
+                rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2],
+                                       host=host, name="race_stress")
+                assert rep.ok(), f"thr {thr} chunk {chunk}: {rep}"
+
+
 def test_the_stress_build_delays(stress_lib):
     """The delays are really there: the same one-block-chunk call takes
     clearly longer through the stress build than through the library."""
