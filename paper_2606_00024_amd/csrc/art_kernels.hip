@@ -785,16 +785,40 @@ __device__ int lookback_once(const KernelParams& P, int gidx, int me, uint32_t n
 
 // States whose data sits in the workspace records: the flag goes out once
 // the record stores have completed.
+// Summaries of consecutive chunks compose (entering run 0 throughout):
+// A then B has the blocks of both, leads with A's lead (extended by B's if A
+// is stable throughout), trails with B's trail (extended by A's if B is),
+// and reaches the patience first inside A, else where A's trailing run and
+// B's leading run together reach it, else inside B.  Folding a state with
+// A then B equals folding it with the composition (the same integers).
+__device__ __forceinline__ StabSummary seg_combine(StabSummary a, StabSummary b, int patience) {
+  StabSummary r;
+  r.len = a.len + b.len;
+  r.lead = a.lead == a.len ? a.len + b.lead : a.lead;
+  r.trail = b.trail == b.len ? b.len + a.trail : b.trail;
+  if (a.fis >= 0) r.fis = a.fis;
+  else if (b.lead > 0 && (int64_t)a.trail + b.lead >= patience) r.fis = a.len + (patience - a.trail) - 1;
+  else if (b.fis >= 0) r.fis = a.len + b.fis;
+  else r.fis = -1;
+  return r;
+}
+
 // Stability state on entering chunk `me` of group gidx: the nearest chunk j
-// before it that published its stability state, with the summaries of the
-// chunks between folded forward (every chunk between must have published
-// its summary).  Flags are read 64 per poll, and when j lies within the
-// first 64 chunks back no further read is needed.  Returns false when a
-// stop before `me` has been announced or the spin limit is reached.
+// before it that published its stability state, folded with the summaries
+// of the chunks between (every chunk between must have published its
+// summary).  One backward pass, 64 flags per read (lane u holds chunk
+// hi - u): each complete window's summaries are composed across the lanes
+// in six shuffle steps and put in front of the composition of the later
+// windows.  A flag read once at its summary may later show the chunk's own
+// state, which is the fold of every chunk up to it, so the summary already
+// used gives the same integers.  Returns false when a stop before `me` has
+// been announced or the spin limit is reached.
 __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState& x, int lane) {
   const uint64_t* flags = P.flags + (int64_t)gidx * P.max_chunks;
-  int hi = me - 1, j = -1;
+  StabSummary acc{0, 0, 0, -1};  // composition of the chunks after the window
+  int hi = me - 1, j = -1;       // j: the chunk that holds the state, if any
   uint32_t it = 0;
+  x = StabState{0, 0, 0, 0};
   while (hi >= 0) {
     const int idx = hi - lane;
     const uint64_t v = idx >= 0 ? ld_relaxed(flags + idx) : 0ull;
@@ -803,48 +827,50 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
     const uint64_t have_sum = __ballot(idx < 0 || st >= kStabSummary);
     const int first = have_st ? __ffsll((unsigned long long)have_st) - 1 : 64;
     const uint64_t need = first >= 64 ? ~0ull : ((1ull << first) - 1ull);
-    if ((have_sum & need) == need) {
-      if (hi == me - 1 && (first < 64 || hi < 64)) {
-        // everything needed is in this first window: chunk hi - u is lane u
-        const uint32_t pl = flag_payload(v);
-        x = StabState{0, 0, 0, 0};
-        if (first < 64) x = unpack_stab(__builtin_amdgcn_readlane(pl, first));
-        const int top = first < 64 ? first : hi + 1;
-        for (int u = top - 1; u >= 0; --u)
-          x = stab_fold(x, unpack_summary(__builtin_amdgcn_readlane(pl, u)), chunk_start(P, hi - u), P.patience);
-        return true;
-      }
-      if (first < 64) {
-        j = hi - first;
-        break;
-      }
-      hi -= 64;  // 64 summaries and no state among them: look further back
+    if ((have_sum & need) != need) {
+      if (stop_announced_before(P, gidx, me)) return false;
+      if (wait_expired(P, ++it)) return false;
+      __builtin_amdgcn_s_sleep(2);
       continue;
     }
-    if (stop_announced_before(P, gidx, me)) return false;
-    if (wait_expired(P, ++it)) return false;
-    __builtin_amdgcn_s_sleep(2);
-  }
-  // the state of chunk j (none when j = -1), then the chunks after it, 64
-  // per read.  The scan saw every one of them at least at its summary, but
-  // each read here may find a chunk that has meanwhile published its own
-  // stability state, whose payload replaced the summary in the flag word.
-  // Such a state is the fold over every chunk up to it, so the fold restarts
-  // from it: the same exact integer result either way.
-  stress_delay(P, gidx, me, 16);
-  x = StabState{0, 0, 0, 0};
-  if (j >= 0) x = unpack_stab(flag_payload(ld_relaxed(flags + j)));
-  for (int i0 = j + 1; i0 < me; i0 += 64) {
-    const int n = min(64, me - i0);
-    const uint64_t v = lane < n ? ld_relaxed(flags + i0 + lane) : 0ull;
+    stress_delay(P, gidx, me, 16);
+    // the window's summaries (lanes below `first` that hold a chunk), in
+    // chunk order: lane u + d holds the earlier chunk.  Within a window every
+    // count is below 2^11, so a summary travels as two words: lead | trail
+    // << 16 and len | (fis + 1) << 16.
     const uint32_t pl = flag_payload(v);
-    const uint64_t is_state = __ballot(lane < n && flag_state(v, P.epoch) >= kStabInclusive);
-    for (int u = 0; u < n; ++u) {
-      const uint32_t w = __builtin_amdgcn_readlane(pl, u);
-      if ((is_state >> u) & 1ull) x = unpack_stab(w);
-      else x = stab_fold(x, unpack_summary(w), chunk_start(P, i0 + u), P.patience);
+    uint32_t w0 = 0u, w1 = 0u;
+    if (lane < first && idx >= 0) {
+      const StabSummary y = unpack_summary(pl);
+      w0 = (uint32_t)y.lead | ((uint32_t)y.trail << 16);
+      w1 = (uint32_t)y.len | ((uint32_t)(y.fis + 1) << 16);
     }
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t e0 = __shfl_down(w0, d), e1 = __shfl_down(w1, d);
+      if ((lane & (2 * d - 1)) == 0 && lane + d < 64) {
+        const StabSummary c = seg_combine(
+            StabSummary{(int32_t)(e0 & 0xffffu), (int32_t)(e0 >> 16), (int32_t)(e1 & 0xffffu), (int32_t)(e1 >> 16) - 1},
+            StabSummary{(int32_t)(w0 & 0xffffu), (int32_t)(w0 >> 16), (int32_t)(w1 & 0xffffu), (int32_t)(w1 >> 16) - 1},
+            P.patience);
+        w0 = (uint32_t)c.lead | ((uint32_t)c.trail << 16);
+        w1 = (uint32_t)c.len | ((uint32_t)(c.fis + 1) << 16);
+      }
+    }
+    w0 = __builtin_amdgcn_readfirstlane(w0);
+    w1 = __builtin_amdgcn_readfirstlane(w1);
+    const StabSummary wsum{(int32_t)(w0 & 0xffffu), (int32_t)(w0 >> 16), (int32_t)(w1 & 0xffffu),
+                           (int32_t)(w1 >> 16) - 1};
+    acc = seg_combine(wsum, acc, P.patience);
+    if (first < 64) {
+      x = unpack_stab(__builtin_amdgcn_readlane(pl, first));
+      j = hi - first;
+      break;
+    }
+    hi -= 64;
   }
+  // the summaries after chunk j (after none: from chunk 0 on)
+  x = stab_fold(x, acc, chunk_start(P, j + 1), P.patience);
   return true;
 }
 
@@ -1466,7 +1492,9 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
 // only once a buffer is free, and every wait targets a chunk claimed
 // earlier, so the launch always makes progress.
 template <int G, bool PH>
-__global__ void __launch_bounds__(kThreads) art_decode_kernel(const KernelParams P) {
+// (groups of 16 heads need the bound to keep two workgroups per CU; for
+// the smaller groups the compiler's own choice was faster)
+__global__ void __launch_bounds__(kThreads, G >= 16 ? 2 : 1) art_decode_kernel(const KernelParams P) {
   // the dynamic buffers must start 16-byte aligned (128-bit LDS accesses):
   // the static block below is a multiple of 16 bytes
   extern __shared__ __align__(16) float smem[];
