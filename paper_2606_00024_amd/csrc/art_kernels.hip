@@ -410,8 +410,8 @@ __device__ __forceinline__ int clamp_page(const KernelParams& P, int b, int tok)
 //     part of the very record the tile is about to write when every block
 //     is one tile (nothing reads it before the record is written, and the
 //     LDS so saved holds longer chunks), else through a 4 KiB staging
-//     buffer.  P is split into three bf16 parts (hi +
-//     mid + lo carries 24 significant bits), so P.V keeps fp32 precision.
+//     buffer.  P is split into three bf16 parts (hi + mid + lo carries 24
+//     significant bits), so P.V keeps fp32 precision.
 // The record written to LDS holds the normalised block output
 // sum_j p_hj v_j / l_h [G][128], m_h [G] (base 2) and l_h [G].  pg[n] is the
 // (uniform) physical page of 16-token group n.
@@ -783,8 +783,6 @@ __device__ int lookback_once(const KernelParams& P, int gidx, int me, uint32_t n
   return -1;
 }
 
-// States whose data sits in the workspace records: the flag goes out once
-// the record stores have completed.
 // Summaries of consecutive chunks compose (entering run 0 throughout):
 // A then B has the blocks of both, leads with A's lead (extended by B's if A
 // is stable throughout), trails with B's trail (extended by A's if B is),
@@ -874,6 +872,8 @@ __device__ bool stab_entering(const KernelParams& P, int gidx, int me, StabState
   return true;
 }
 
+// States whose data sits in the workspace records: the flag goes out once
+// the record stores have completed.
 __device__ __forceinline__ void publish(const KernelParams& P, int gidx, int k, uint32_t state, int lane) {
   stress_delay(P, gidx, k, 1);
   stores_complete();
