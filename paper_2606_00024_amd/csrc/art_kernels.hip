@@ -1122,7 +1122,7 @@ __device__ void resolve_heads(const KernelParams& P, int gidx, int k, const Grou
   if (__all(!mine || (sm.lead == 0 && sm.fis < 0)) && k != n_chunks - 1) return;
 
   // entering state per head: the nearest published state, then the
-  // summaries after it, folded in order (four chunks' words in flight)
+  // summaries after it
   stress_delay(P, gidx, k, 11);
   const int j = stab_scan(P, gidx, k, lane);
   if (j == -2) return;
@@ -1133,20 +1133,48 @@ __device__ void resolve_heads(const KernelParams& P, int gidx, int k, const Grou
     x.stopped = ld_coh_i32(w + 4);
     x.run = ld_coh_i32(w + 5);
   }
-  for (int i0 = j + 1; i0 < k; i0 += 4) {
-    const int n = min(4, k - i0);
-    int32_t v[4][4];
+  if (k - (j + 1) <= 4 * G) {
+    // a short way back (up to one round trip per head either way): every
+    // head folds its own summaries, lane h head h, four chunks' words in
+    // flight
+    for (int i0 = j + 1; i0 < k; i0 += 4) {
+      const int n = min(4, k - i0);
+      int32_t v[4][4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (mine && u < n) {
-        const int32_t* w = head_area(P, gidx, i0 + u, G) + lane * 8;
+      for (int u = 0; u < 4; ++u)
+        if (mine && u < n) {
+          const int32_t* w = head_area(P, gidx, i0 + u, G) + lane * 8;
 #pragma unroll
-        for (int f = 0; f < 4; ++f) v[u][f] = ld_coh_i32(w + f);
+          for (int f = 0; f < 4; ++f) v[u][f] = ld_coh_i32(w + f);
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (mine && u < n)
+          x = stab_fold(x, StabSummary{v[u][0], v[u][1], v[u][2], v[u][3]}, chunk_start(P, i0 + u), P.patience);
+    }
+  } else {
+    // a long way back (the last chunk of a traversal with no stop before):
+    // 64 chunks per read (lane u: chunk i0 + u), composed across the lanes
+    // for each head in turn
+    for (int i0 = j + 1; i0 < k; i0 += 64) {
+      const bool in = lane < k - i0;
+      const int32_t* wc = head_area(P, gidx, in ? i0 + lane : i0, G);
+      const int t_win = chunk_start(P, i0);
+      for (int h = 0; h < G; ++h) {
+        StabSummary c{0, 0, 0, -1};
+        if (in) c = StabSummary{ld_coh_i32(wc + h * 8), ld_coh_i32(wc + h * 8 + 1), ld_coh_i32(wc + h * 8 + 2),
+                                ld_coh_i32(wc + h * 8 + 3)};
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const StabSummary e{__shfl_down(c.lead, d), __shfl_down(c.trail, d), __shfl_down(c.len, d),
+                              __shfl_down(c.fis, d)};
+          if ((lane & (2 * d - 1)) == 0 && lane + d < 64) c = seg_combine(c, e, P.patience);
+        }
+        const StabSummary comp{__builtin_amdgcn_readfirstlane(c.lead), __builtin_amdgcn_readfirstlane(c.trail),
+                               __builtin_amdgcn_readfirstlane(c.len), __builtin_amdgcn_readfirstlane(c.fis)};
+        if (lane == h) x = stab_fold(x, comp, t_win, P.patience);
       }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (mine && u < n)
-        x = stab_fold(x, StabSummary{v[u][0], v[u][1], v[u][2], v[u][3]}, chunk_start(P, i0 + u), P.patience);
+    }
   }
   const StabState y = mine ? stab_fold(x, sm, t0, P.patience) : x;
   if (mine) {
