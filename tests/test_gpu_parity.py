@@ -375,3 +375,35 @@ def test_no_detector_is_full_attention(case):
     rep = compare_workload(wl, gpu, tau=0.0, phi=1e-4, patience=5, name="no_detector")
     _say("  ", rep)
     assert rep.ok(), str(rep)
+
+
+# Long patience on mostly stable traversals: the stops lie well over 64
+# chunks into the traversal at one-block chunks, so the stability state on
+# entering a chunk composes several windows of non-trivial summaries (runs
+# that cross many chunks), in the group reading and in the per-head one.
+LONG_PATIENCE = [
+    # seed, Hkv, g, seq_len, (tau, phi, patience)
+    (97, 2, 8, 12000, (0.05, 1e-2, 60)),
+    (98, 2, 4, 16000, (0.1, 0.02, 100)),
+    (98, 2, 4, 16000, (0.05, 1e-2, 60)),
+]
+
+
+@pytest.mark.parametrize("case", LONG_PATIENCE, ids=[f"s{c[0]}-p{c[4][2]}" for c in LONG_PATIENCE])
+def test_long_patience_composition(case):
+    from parity import compare_per_head
+    seed, hkv, g, L, (tau, phi, p) = case
+    wl = small_workload(seed, batch=1, kv_heads=hkv, group=g, seq_len=L, needles=2)
+    for name in ("q", "k_cache", "v_cache", "page_table", "seq_lens"):
+        setattr(wl, name, getattr(wl, name).to(DEV))
+    host = host_copy(wl)
+    for chunk in (1, 2, 0):
+        _say(f"  long patience s{seed} p={p} chunk={chunk}")
+        gpu = api.decode_workload(wl, tau=tau, phi=phi, patience=p, chunk_blocks=chunk)
+        torch.cuda.synchronize()
+        rep = compare_workload(wl, gpu, tau=tau, phi=phi, patience=p, host=host, name="long_patience")
+        assert rep.ok(), f"chunk {chunk}: {rep}"
+    gpu = api.decode_workload(wl, tau=tau, phi=phi, patience=p, chunk_blocks=1, per_head_stop=True)
+    torch.cuda.synchronize()
+    rep = compare_per_head(wl, gpu, tau=tau, phi=phi, patience=p, host=host, name="long_patience_per_head")
+    assert rep.ok(), f"per head: {rep}"
