@@ -331,6 +331,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t record_rsrc(const KernelParams
                                            P.max_chunks * 2 * P.record_floats * 4, 0x00020000);
 }
 
+// Layout of a workspace record (G*kD + 2G floats).  Head h's outputs fill
+// floats h*kD .. h*kD + 127, first the first halves of the sixteen lanes'
+// eight coordinates (lane c: dims 8c .. 8c+3 at 4c), then the second halves
+// (dims 8c+4 .. 8c+7 at 64 + 4c), so that each store instruction covers
+// whole 64-byte segments (256 contiguous bytes per head) and each segment
+// leaves the L2 once, not once per half; m and L of head h follow at G*kD + h
+// and G*kD + G + h.
 template <int G>
 __device__ __forceinline__ void publish_state(__amdgpu_buffer_rsrc_t rs, int rec_off, const State<G>& s,
                                               int lane) {
@@ -339,9 +346,9 @@ __device__ __forceinline__ void publish_state(__amdgpu_buffer_rsrc_t rs, int rec
   for (int k = 0; k < Cfg<G>::HPL; ++k) {
     const int h = r + 4 * k;
     if (h < G) {
-      const int off = (rec_off + h * kD + c * 8) * 4;
+      const int off = (rec_off + h * kD + c * 4) * 4;
       __builtin_amdgcn_raw_buffer_store_b128(f32x4{s.o[k][0], s.o[k][1], s.o[k][2], s.o[k][3]}, rs, off, 0, kCoherent);
-      __builtin_amdgcn_raw_buffer_store_b128(f32x4{s.o[k][4], s.o[k][5], s.o[k][6], s.o[k][7]}, rs, off + 16, 0, kCoherent);
+      __builtin_amdgcn_raw_buffer_store_b128(f32x4{s.o[k][4], s.o[k][5], s.o[k][6], s.o[k][7]}, rs, off + 256, 0, kCoherent);
       if (c == 0) {
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s.m[k]), rs, (rec_off + G * kD + h) * 4, 0, kCoherent);
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s.L[k]), rs, (rec_off + G * kD + G + h) * 4, 0, kCoherent);
@@ -357,9 +364,9 @@ __device__ __forceinline__ void fetch_state(__amdgpu_buffer_rsrc_t rs, int rec_o
   for (int k = 0; k < Cfg<G>::HPL; ++k) {
     int h = r + 4 * k;
     if (h >= G) h = 0;
-    const int off = (rec_off + h * kD + c * 8) * 4;
+    const int off = (rec_off + h * kD + c * 4) * 4;
     const f32x4 x0 = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kCoherent);
-    const f32x4 x1 = __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, kCoherent);
+    const f32x4 x1 = __builtin_amdgcn_raw_buffer_load_b128(rs, off + 256, 0, kCoherent);
     s.o[k][0] = x0[0]; s.o[k][1] = x0[1]; s.o[k][2] = x0[2]; s.o[k][3] = x0[3];
     s.o[k][4] = x1[0]; s.o[k][5] = x1[1]; s.o[k][6] = x1[2]; s.o[k][7] = x1[3];
     s.m[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, (rec_off + G * kD + h) * 4, 0, kCoherent));
