@@ -1321,24 +1321,21 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     for (int u = 0; u < FW; ++u)
       if (u < n) merge<G, false>(pre, a[u]);
   }
-  // this chunk's inclusive state; its flag goes out during the replay
+  // this chunk's inclusive state, published before the replay: the next
+  // chunks wait for it (measured: raising its flag only after the replay's
+  // first blocks, to overlap the stores' completion, was 0.5 % slower)
   {
     State<G> inc = pre;
     merge<G, false>(inc, agg);
     publish_state<G>(rs, rec_inc, inc, lane);
+    publish(P, gidx, k, kInclusive, lane);
     if (P.no_detector) {
       // no stability test (the detector-free baseline): later chunks need
       // only the inclusive state, and the last chunk holds the output
-      publish(P, gidx, k, kInclusive, lane);
       if (k == n_chunks - 1) write_outputs<G>(P, b, kvh, inc, T, lane);
       return;
     }
   }
-  bool incl_pending = true;
-  auto raise_inclusive = [&]() {
-    publish(P, gidx, k, kInclusive, lane);
-    incl_pending = false;
-  };
 
   // Replay the chunk's blocks from the prefix with the stability test.
   // Blocks go in batches of NB: the merges run in order (each needs the
@@ -1419,7 +1416,6 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
           }
         }
       }
-      if (incl_pending) raise_inclusive();
 #pragma unroll
       for (int u = 0; u < NB; ++u)
 #pragma unroll
