@@ -324,6 +324,7 @@ __device__ __forceinline__ void read_state(const float* rec, State<G>& s, int la
 // area with the sc1 cache policy: agent-coherent 16-byte accesses whose
 // completion the compiler tracks like any other load or store.
 constexpr int kCoherent = 16;  // buffer cache policy: sc1
+constexpr int kLookFirstPasses = 5;  // look-back passes before a chunk publishes its aggregate
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t record_rsrc(const KernelParams& P, int gidx) {
   const float* base = P.records + (int64_t)gidx * P.max_chunks * 2 * P.record_floats;
@@ -1290,7 +1291,14 @@ __device__ void resolve_chunk(const KernelParams& P, int gidx, int k, const Grou
     // are those of many groups of 8, and the extra code alone measurably
     // slowed the instances for smaller groups)
     if (G >= 8 && P.look_first) {
+      // a few passes, a short sleep apart: a prefix that completes within
+      // them spares this chunk its aggregate record (measured: one pass and
+      // four more 0.3-0.6 % faster than one, sixteen no better, 32 slower)
       j = lookback_once(P, gidx, k, kAggregate, kInclusive, lane);
+      for (int pass = 1; j == -3 && pass < kLookFirstPasses; ++pass) {
+        __builtin_amdgcn_s_sleep(8);
+        j = lookback_once(P, gidx, k, kAggregate, kInclusive, lane);
+      }
       if (j == -3) {
         publish_state<G>(rs, rec_agg, agg, lane);
         publish(P, gidx, k, kAggregate, lane);
