@@ -115,7 +115,7 @@ def build(verbose: bool = False, extra=()) -> str:
         STRESS_LIB: [_obj("art_kernels_stress")] + dev[1:] + [_obj(HOST_SOURCE)],
         BENCH_LIB: [_obj("art_read_peak.hip")],
         # the AddressSanitizer runtime is not linked in: the process that
-        # loads this build preloads gcc's libasan (tests/test_host_asan.py)
+        # loads this library preloads gcc's libasan (tests/test_host_asan.py)
         ASAN_LIB: dev + [_obj("art_api_asan")],
     }
     _run_all([(os.path.basename(lib), [cc, f"--offload-arch={ARCH}", "-shared", "-o", lib + ".tmp", *objs])

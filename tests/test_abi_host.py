@@ -213,7 +213,7 @@ def test_empty_batch_is_a_no_op(lib):
 
 
 def test_graft_entry_builds(lib):
-    import __graft_entry__  # noqa: F401  (import only: build() is exercised by the driver)
+    import __graft_entry__  # noqa: F401  (import only: build() recompiles every library)
 
 
 def _lopts(**kw):
