@@ -286,6 +286,7 @@ art_status art_workspace_status(const void* workspace, size_t workspace_bytes,
  *         ART_SCORE_QUERY_BOUND: max over the group's query heads of
  *                                sum_d max(q_d * min_j k_jd, q_d * max_j k_jd),
  *                                which bounds q . k_j over the block from above.
+ *       Keys and queries that hold a NaN give unspecified scores.
  *   ART_LIST_STREAMING  a cache of sink tokens plus a recent window
  *       (pattern-based policies).  Blocks 0 .. sink_blocks-1 come first, in
  *       increasing order, so that a stop never drops the sinks.  Then come the

@@ -209,41 +209,39 @@ __device__ __forceinline__ void stream_tiles(const ListParams& P, const int* s_l
 }
 
 // Lane j sums the 128 squares of token j in dimension order: the tile goes
-// through LDS, 32 tokens at a time.
+// through LDS (64 rows per wavefront).  Each square of a bf16 value is exact
+// in fp64, so the fused multiply-add rounds once per term, as the separate
+// product and sum would.  Rows past the block's end hold its first row
+// again (load_tile), which leaves the maximum unchanged.
+constexpr int kKeyNormLds = 4 * 64 * kRowPitch;   // bytes per workgroup
+
 __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P) {
     extern __shared__ __align__(16) unsigned char tiles[];
     __shared__ __align__(16) int s_len[kListLenCache];
     cache_lens(P, s_len);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    unsigned char* tile = tiles + w * 32 * kRowPitch;
+    unsigned char* tile = tiles + w * 64 * kRowPitch;
     double best = -1.0;   // below any sum of squares
     stream_tiles(P, s_len, [](const TilePos&) {},
-        [&](const TilePos& t, const u32x4_l (&v)[kTileLoads]) {
+        [&](const TilePos&, const u32x4_l (&v)[kTileLoads]) {
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                // loads 8*half .. 8*half+7 hold tokens 32*half .. 32*half+31
+            for (int i = 0; i < kTileLoads; ++i)
+                *reinterpret_cast<u32x4_l*>(tile + (4 * i + (lane >> 4)) * kRowPitch + 16 * (lane & 15)) = v[i];
+            wave_lds_fence();
+            const unsigned char* row = tile + lane * kRowPitch;
+            double s = 0.0;
 #pragma unroll
-                for (int i = 0; i < kTileLoads / 2; ++i)
-                    *reinterpret_cast<u32x4_l*>(tile + (4 * i + (lane >> 4)) * kRowPitch + 16 * (lane & 15)) =
-                        v[8 * half + i];
-                wave_lds_fence();
-                if (lane < 32 && t.t0 + 32 * half + lane < t.j1) {
-                    const unsigned char* row = tile + lane * kRowPitch;
-                    double s = 0.0;
+            for (int c = 0; c < 16; ++c) {
+                const u32x4_l x = *reinterpret_cast<const u32x4_l*>(row + 16 * c);
 #pragma unroll
-                    for (int c = 0; c < 16; ++c) {
-                        const u32x4_l x = *reinterpret_cast<const u32x4_l*>(row + 16 * c);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const double x0 = bf16_lo(x[e]), x1 = bf16_hi(x[e]);
-                            s = s + x0 * x0;   // dimension 8c + 2e
-                            s = s + x1 * x1;   // dimension 8c + 2e + 1
-                        }
-                    }
-                    best = fmax(best, s);
+                for (int e = 0; e < 4; ++e) {
+                    const double x0 = bf16_lo(x[e]), x1 = bf16_hi(x[e]);
+                    s = __builtin_fma(x0, x0, s);   // dimension 8c + 2e
+                    s = __builtin_fma(x1, x1, s);   // dimension 8c + 2e + 1
                 }
-                wave_lds_fence();   // the rows are read before they are written again
             }
+            best = fmax(best, s);
+            wave_lds_fence();   // the rows are read before they are written again
         },
         [&](const TilePos& t) {
             // every lane stores the same value (no branch around the store)
@@ -256,15 +254,65 @@ __global__ void __launch_bounds__(256) score_key_norm_kernel(const ListParams P)
 // its loads cover; at the end of a block the four lane rows are combined,
 // the per-dimension terms of every query head go to LDS, and lane h sums
 // head h's 128 terms in order.
+//
+// The extremes are taken on the raw bf16 words, two dimensions per
+// instruction, with no conversion: a bf16 is sign and magnitude, so over a
+// set of values the largest is the largest as a signed 16-bit integer when
+// that one is non-negative and otherwise (all negative) the smallest as a
+// signed integer; the smallest is the largest as an unsigned integer when
+// any sign bit is set and otherwise the smallest as an unsigned integer.
+// Four packed extremes per word (signed and unsigned, largest and
+// smallest) give both.  This holds for every value but NaN (keys hold
+// none) and treats -0 as the smallest negative, which changes no term:
+// q * (+-0) is a zero either way and adding a zero of either sign to the
+// running sum, which starts at +0, gives the same bits.  Rows past the
+// block's end hold its first row again (load_tile), which changes no
+// extreme.
+typedef short s16x2_l __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2_l __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t pk_smax(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2_l, a),
+                                                                  __builtin_bit_cast(s16x2_l, b)));
+}
+__device__ __forceinline__ uint32_t pk_smin(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(s16x2_l, a),
+                                                                  __builtin_bit_cast(s16x2_l, b)));
+}
+__device__ __forceinline__ uint32_t pk_umax(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2_l, a),
+                                                                  __builtin_bit_cast(u16x2_l, b)));
+}
+__device__ __forceinline__ uint32_t pk_umin(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(u16x2_l, a),
+                                                                  __builtin_bit_cast(u16x2_l, b)));
+}
+
+// The value (as a float) of the largest and the smallest bf16 of one half
+// (shift 0: low, 16: high) of the four packed extremes.
+__device__ __forceinline__ void half_extremes(uint32_t smax, uint32_t smin, uint32_t umax, uint32_t umin,
+                                              int shift, float& lo, float& hi) {
+    const uint32_t sx = (smax >> shift) & 0xffffu, sn = (smin >> shift) & 0xffffu;
+    const uint32_t ux = (umax >> shift) & 0xffffu, un = (umin >> shift) & 0xffffu;
+    hi = __uint_as_float((sx < 0x8000u ? sx : sn) << 16);
+    lo = __uint_as_float((ux >= 0x8000u ? ux : un) << 16);
+}
+
 template <int G>
 __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams P) {
     __shared__ double terms[4][G][128];
     __shared__ __align__(16) int s_len[kListLenCache];
     cache_lens(P, s_len);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    float lo[8], hi[8];
+    // word e of the lane's 16 bytes: dimensions 8c + 2e (low half), 8c + 2e + 1
+    uint32_t smax[4], smin[4], umax[4], umin[4];
+    auto reset = [&]() {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }
+        for (int e = 0; e < 4; ++e) {
+            smax[e] = 0x80008000u; smin[e] = 0x7fff7fffu; umax[e] = 0u; umin[e] = 0xffffffffu;
+        }
+    };
+    reset();
     // lane row r holds dimensions 8*(lane & 15) .. +7 of query heads r, r + 4, ...
     constexpr int QR = (G + 3) / 4;
     u32x4_l qw[QR];
@@ -278,25 +326,33 @@ __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams
                     P.q + ((int64_t)t.b * P.num_q_heads + t.kvh * G + h) * kHeadDim)[c];
             }
         },
-        [&](const TilePos& t, const u32x4_l (&v)[kTileLoads]) {
+        [&](const TilePos&, const u32x4_l (&v)[kTileLoads]) {
 #pragma unroll
             for (int i = 0; i < kTileLoads; ++i) {
-                if (t.t0 + 4 * i + (lane >> 4) < t.j1) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float x0 = __uint_as_float(v[i][e] << 16), x1 = __uint_as_float(v[i][e] & 0xffff0000u);
-                        lo[2 * e] = fminf(lo[2 * e], x0); hi[2 * e] = fmaxf(hi[2 * e], x0);
-                        lo[2 * e + 1] = fminf(lo[2 * e + 1], x1); hi[2 * e + 1] = fmaxf(hi[2 * e + 1], x1);
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    smax[e] = pk_smax(smax[e], v[i][e]); smin[e] = pk_smin(smin[e], v[i][e]);
+                    umax[e] = pk_umax(umax[e], v[i][e]); umin[e] = pk_umin(umin[e], v[i][e]);
                 }
             }
         },
         [&](const TilePos& t) {
             // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same dimensions
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                lo[e] = fminf(lo[e], __shfl_xor(lo[e], 16)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 16));
-                lo[e] = fminf(lo[e], __shfl_xor(lo[e], 32)); hi[e] = fmaxf(hi[e], __shfl_xor(hi[e], 32));
+            for (int e = 0; e < 4; ++e) {
+#pragma unroll
+                for (int o = 16; o <= 32; o <<= 1) {
+                    smax[e] = pk_smax(smax[e], (uint32_t)__shfl_xor((int)smax[e], o));
+                    smin[e] = pk_smin(smin[e], (uint32_t)__shfl_xor((int)smin[e], o));
+                    umax[e] = pk_umax(umax[e], (uint32_t)__shfl_xor((int)umax[e], o));
+                    umin[e] = pk_umin(umin[e], (uint32_t)__shfl_xor((int)umin[e], o));
+                }
+            }
+            float lo[8], hi[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                half_extremes(smax[e], smin[e], umax[e], umin[e], 0, lo[2 * e], hi[2 * e]);
+                half_extremes(smax[e], smin[e], umax[e], umin[e], 16, lo[2 * e + 1], hi[2 * e + 1]);
             }
             // lane row r writes the terms of heads r, r + 4, ...
 #pragma unroll
@@ -319,8 +375,7 @@ __global__ void __launch_bounds__(256) score_query_bound_kernel(const ListParams
             }
             P.scores[(int64_t)t.gidx * P.max_blocks + t.blk] = wave_max(s);
             wave_lds_fence();   // the terms are read before the next block writes them
-#pragma unroll
-            for (int e = 0; e < 8; ++e) { lo[e] = INFINITY; hi[e] = -INFINITY; }
+            reset();
         });
 }
 
@@ -605,7 +660,7 @@ art_status art_build_block_list(const art_decode_shape* shape, const art_list_op
     if (importance && (int64_t)groups * mb > 0) {
         const int64_t waves = (int64_t)groups * mb;
         if (opts->score_kind == ART_SCORE_KEY_NORM) {
-            if (launch_persistent(score_key_norm_kernel, waves, 4 * 32 * kRowPitch, stream, P) != hipSuccess)
+            if (launch_persistent(score_key_norm_kernel, waves, kKeyNormLds, stream, P) != hipSuccess)
                 return ART_ERR_HIP;
         } else {
             hipError_t e;

@@ -121,6 +121,36 @@ def test_equal_scores_and_longest_sequences():
         _compare(wl, host, OL.IMPORTANCE, OL.KEY_NORM, budget, sinks, last)
 
 
+def test_special_key_values():
+    """Keys whose channels take every sign case of the extremes: channels
+    negative on every token of every block, positive on every token, zeros
+    of both signs (whole blocks of -0 too), bf16 subnormals, and magnitudes
+    near 1e30; the extremes and the squares are compared bit for bit with
+    the oracle's."""
+    rng = np.random.default_rng(69)
+    host = small_workload(69, batch=2, kv_heads=2, group=4, seq_len=(3000, 1000), block_size=64,
+                          page_size=64, needles=0)
+    k = host.k_cache.float()
+    n_pages, hkv, ps, d = k.shape
+    k[..., 0:16] = -k[..., 0:16].abs() - 1e-3
+    k[..., 16:32] = k[..., 16:32].abs() + 1e-3
+    zeros = torch.from_numpy(rng.integers(0, 2, size=(n_pages, hkv, ps, 16)).astype(np.float32))
+    k[..., 32:48] = torch.where(zeros > 0, torch.tensor(-0.0), torch.tensor(0.0))
+    k[: n_pages // 2, :, :, 40:48] = -0.0
+    sub = torch.from_numpy(rng.integers(1, 127, size=(n_pages, hkv, ps, 16)).astype(np.float32))
+    sign = torch.from_numpy(rng.choice([-1.0, 1.0], size=(n_pages, hkv, ps, 16)).astype(np.float32))
+    k[..., 48:64] = sign * sub * 2.0 ** -133          # bf16 subnormals (exact in float32)
+    k[..., 64:80] = k[..., 64:80] * 1e30
+    k[: n_pages // 3, :, :, 80:96] = -7.0             # one value on every token
+    host.k_cache = k.to(torch.bfloat16)
+    kb = host.k_cache.float()
+    assert bool((kb[..., 48:64] != 0).all()) and bool((kb[..., 48:64].abs() < 2.0 ** -126).all())
+    assert bool(torch.signbit(kb[..., 32:48]).any()) and bool((~torch.signbit(kb[..., 32:48])).any())
+    wl = _to_dev(copy.copy(host))
+    for kind in (OL.KEY_NORM, OL.QUERY_BOUND):
+        _compare(wl, host, OL.IMPORTANCE, kind, 20, 1, True)
+
+
 def test_device_lists_drive_the_decode_call():
     """Lists built on the device, then decode over them; the reference is the
     decode oracle over the oracle's lists (the same lists, bit for bit)."""
