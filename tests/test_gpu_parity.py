@@ -105,6 +105,26 @@ def test_small_matrix(case, thr):
 MANY_LENS = tuple(int(x) for x in np.random.default_rng(7).integers(0, 700, 300))
 
 
+@pytest.mark.parametrize("case", [SMALL[0], SMALL[3], SMALL[9]], ids=["s1", "s4", "s10"])
+def test_large_logits(case):
+    """Queries scaled by 6: scores with a standard deviation near 7 and the
+    needles' near 100, so that many of a softmax's terms underflow fp32
+    (exp of a difference below -104) while fp64 keeps them; the online
+    softmax's running maximum and rescaling must keep every state finite."""
+    seed, B, hkv, g, L, bk, ps, order, lists = case
+    wl = small_workload(seed, batch=B, kv_heads=hkv, group=g, seq_len=L, block_size=bk,
+                        page_size=ps, dense_order=order, needles=2)
+    wl.q = (wl.q.float() * 6.0).to(torch.bfloat16)
+    if lists:
+        wl.block_list, wl.block_list_len = random_lists(wl, seed, fraction=0.6)
+    wl = _to_dev(wl)
+    for thr in THRESHOLDS[:3]:
+        gpu = _run(wl, *thr)
+        rep = compare_workload(wl, gpu, tau=thr[0], phi=thr[1], patience=thr[2], name="large_logits")
+        _say("  ", rep)
+        assert rep.ok(), str(rep)
+
+
 @pytest.mark.parametrize("lists", [False, True], ids=["dense", "lists"])
 @pytest.mark.parametrize("thr", THRESHOLDS[:3], ids=["cfg", "relaxed", "off"])
 def test_batch_beyond_the_length_cache(lists, thr):
