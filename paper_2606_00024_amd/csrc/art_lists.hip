@@ -395,6 +395,41 @@ hipError_t launch_persistent(Kernel kernel, int64_t items, size_t lds, hipStream
     return hipGetLastError();
 }
 
+// The value that lane (lane ^ S) holds, S one of 1, 2, 4, 8, 16, 32, by
+// the cross-lane moves of the vector ALU instead of a round trip through
+// the LDS unit: quad permutes for 1 and 2, rotations within a row of 16
+// lanes for 4 and 8 (row_ror:n hands lane i the value of lane i - n of
+// its row), and the swaps of 16- and 32-lane halves for 16 and 32.
+template <int S>
+__device__ __forceinline__ int xor_lane(int x) {
+    const int lane = threadIdx.x & 63;
+    if constexpr (S == 1) {
+        return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xf, 0xf, false);   // quad_perm [1,0,3,2]
+    } else if constexpr (S == 2) {
+        return __builtin_amdgcn_mov_dpp(x, 0x4E, 0xf, 0xf, false);   // quad_perm [2,3,0,1]
+    } else if constexpr (S == 4) {
+        const int from_above = __builtin_amdgcn_mov_dpp(x, 0x12C, 0xf, 0xf, false);   // row_ror:12
+        const int from_below = __builtin_amdgcn_mov_dpp(x, 0x124, 0xf, 0xf, false);   // row_ror:4
+        return (lane & 4) ? from_below : from_above;
+    } else if constexpr (S == 8) {
+        return __builtin_amdgcn_mov_dpp(x, 0x128, 0xf, 0xf, false);  // row_ror:8
+    } else if constexpr (S == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    } else {
+        static_assert(S == 32, "a power of two up to 32");
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (lane & 32) ? r[0] : r[1];
+    }
+}
+
+template <int S>
+__device__ __forceinline__ double xor_lane(double x) {
+    const long long w = __double_as_longlong(x);
+    const int lo = xor_lane<S>((int)(w & 0xffffffffll)), hi = xor_lane<S>((int)(w >> 32));
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
 // a before b: larger score, then smaller id
 __device__ __forceinline__ bool before(double sa, int ia, double sb, int ib) {
     return sa > sb || (sa == sb && ia < ib);
@@ -430,6 +465,23 @@ __device__ int block_exclusive_scan(int v, int* scratch, int& total) {
     return r;
 }
 
+// One lane's element (k, i) at position pos through the bitonic stages
+// with strides S, S/2, ..., 1 of a run of `size` positions: the lower
+// position of each pair keeps whichever element comes first in a run that
+// puts "before" first (up), the upper one the other; the other runs the
+// other way round.
+template <int S>
+__device__ __forceinline__ void register_stages(double& k, int& i, bool up, int lane) {
+    const double pk = xor_lane<S>(k);
+    const int pi = xor_lane<S>(i);
+    const bool lower = (lane & S) == 0;
+    if ((lower == up) != before(k, i, pk, pi)) {
+        k = pk;
+        i = pi;
+    }
+    if constexpr (S > 1) register_stages<S / 2>(k, i, up, lane);
+}
+
 __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P) {
     extern __shared__ __align__(16) unsigned char lds[];
     const int gidx = blockIdx.x, tid = threadIdx.x;
@@ -460,7 +512,7 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
     // through LDS, one pair per thread and a workgroup barrier each.  Stages
     // below a stride of 64 never leave a 64-position segment: they run in
     // registers, each wavefront taking whole segments (lane l holds position
-    // 64 s + l) and exchanging with lane l ^ stride by shuffles, so that a
+    // 64 s + l) and exchanging with lane l ^ stride (xor_lane), so that a
     // segment is read and written once per run of such stages.  Sizes up to
     // 64 have no other stages and run in a single pass.
     const int wave = tid >> 6, lane = tid & 63;
@@ -471,18 +523,13 @@ __global__ void __launch_bounds__(kListThreads) select_kernel(const ListParams P
             int i = pos < N ? id[pos] : 0x7fffffff;
             for (int size = size_from; size <= size_to; size <<= 1) {
                 const bool up = (pos & size) == 0;   // this run sorts "before" first
-                for (int stride = min(size >> 1, 32); stride > 0; stride >>= 1) {
-                    const double pk = __shfl_xor(k, stride);
-                    const int pi = __shfl_xor(i, stride);
-                    const bool lower = (lane & stride) == 0;
-                    const bool mine_first = before(k, i, pk, pi);
-                    // in a run that puts "before" first, the lower position
-                    // keeps whichever element comes first and the upper one
-                    // the other; the other runs the other way round
-                    if ((lower == up) != mine_first) {
-                        k = pk;
-                        i = pi;
-                    }
+                switch (min(size >> 1, 32)) {
+                    case 32: register_stages<32>(k, i, up, lane); break;
+                    case 16: register_stages<16>(k, i, up, lane); break;
+                    case 8: register_stages<8>(k, i, up, lane); break;
+                    case 4: register_stages<4>(k, i, up, lane); break;
+                    case 2: register_stages<2>(k, i, up, lane); break;
+                    default: register_stages<1>(k, i, up, lane); break;
                 }
             }
             if (pos < N) {
