@@ -280,8 +280,10 @@ def measure(wl, tau, phi, pat, steps, warmup, copies, chunk_blocks=0, no_detecto
         "alg_bytes_per_launch": alg,
     }
     out = run.out.clone() if keep_out else None
+    # the caching allocator keeps the freed buffers for the next mode's
+    # runner: memory handed back to the driver and mapped again made the
+    # launches that followed up to 1-2 % slower than steady state
     del run
-    torch.cuda.empty_cache()
     return res, out
 
 
